@@ -1,0 +1,392 @@
+/*
+ * ft_oracle.c -- plain, slow, fp64 CPU oracle for the W4A4G4 triple-branch
+ * linear layer (FourTune, arXiv 2607.05711).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the yardstick the HIP library is
+ * checked against.  Only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg may load it.  It shares no code, header, table or helper
+ * with the GPU library (paper_2607_05711_amd/csrc), and the GPU library never
+ * calls it.
+ *
+ * Everything is computed in IEEE double precision with straightforward loops:
+ * no blocking, no SIMD intrinsics, no BLAS, no fused reordering.  OpenMP only
+ * splits independent output rows across threads; every sum runs in index order.
+ *
+ * What is computed (paper: Section 3, "Method"):
+ *   - Q(.)  block-wise 4-bit quantization.  The paper states NVFP4 (Sec. 3.1)
+ *     and cites the OCP Microscaling formats (Sec. 2.3, Rouhani et al. 2023).
+ *     Reading used here: MXFP4 = E2M1 elements with one E8M0 power-of-two
+ *     scale per block; activations and gradients use 1x32 blocks along the
+ *     reduction axis, the frozen weight uses 32x32 tiles so that the same
+ *     codes and scales serve the transposed product (Sec. 3.2).
+ *     The shared exponent follows the Microscaling rule
+ *     e = floor(log2(amax)) - emax(E2M1), emax = 2, clamped to the E8M0 range;
+ *     elements round to the nearest E2M1 value, ties to the even code,
+ *     saturating at 6; the sign bit is copied from the input (also for -0).
+ *   - forward, Eq. (2):  Y = DQ(Q(X)) DQ(Q(W))^T + X L1 L2 + X A B + bias
+ *   - input gradient, Eq. (3):  dX = DQ(Q(G)) DQ(Q(W)) + G (L1 L2)^T + G (A B)^T
+ *   - adapter gradients (Sec. 3.2): dB = (X A)^T G, dA = X^T (G B^T)
+ *   - GELU (tanh form) and its derivative for the MLP pair (Sec. 3.3, MLP fusion).
+ *
+ * The two GEMM entry points also return S = sum over terms of |term| per
+ * output element, the scale against which floating-point parity is judged.
+ *
+ * Build:  gcc -O2 -fopenmp -shared -fPIC ft_oracle.c -o libft_oracle.so -lm
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------ formats */
+
+/* bf16 is the top half of an IEEE binary32; widening to double is exact. */
+static double bf16_value(uint16_t bits)
+{
+    uint32_t u = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* E2M1 magnitudes in code order (OCP Microscaling, FP4 element type). */
+static const double E2M1_MAGNITUDE[8] = {0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0};
+
+/* Value of a 4-bit E2M1 code: bit 3 is the sign. */
+double fto_e2m1_value(int code)
+{
+    double m = E2M1_MAGNITUDE[code & 7];
+    return (code & 8) ? -m : m;
+}
+
+/* Value of an 8-bit E8M0 scale code: 2^(code-127); 0xFF is NaN. */
+double fto_e8m0_value(int code)
+{
+    if (code == 255)
+        return NAN;
+    return ldexp(1.0, code - 127);
+}
+
+/* Shared block exponent from the block's largest magnitude. */
+static int block_exponent(double amax)
+{
+    int ex;
+    int e;
+    if (amax == 0.0)
+        return -127;
+    frexp(amax, &ex);          /* amax = f * 2^ex, f in [0.5, 1): floor(log2 amax) = ex - 1 */
+    e = (ex - 1) - 2;          /* largest E2M1 magnitude is 1.5 * 2^2 */
+    if (e < -127)
+        e = -127;
+    if (e > 127)
+        e = 127;
+    return e;
+}
+
+/* Nearest E2M1 magnitude code to t >= 0; on a tie the even code wins. */
+static int nearest_magnitude_code(double t)
+{
+    int best = 0;
+    double best_d = fabs(t - E2M1_MAGNITUDE[0]);
+    for (int c = 1; c < 8; c++) {
+        double d = fabs(t - E2M1_MAGNITUDE[c]);
+        if (d < best_d || (d == best_d && (c & 1) == 0)) {
+            best_d = d;
+            best = c;
+        }
+    }
+    return best;
+}
+
+/* Quantize n values sharing one scale: writes n 4-bit codes (one per byte of
+ * codes4) and returns the E8M0 scale code. */
+static int quantize_block(const double *v, int n, uint8_t *codes4)
+{
+    double amax = 0.0;
+    for (int i = 0; i < n; i++)
+        if (fabs(v[i]) > amax)
+            amax = fabs(v[i]);
+    int e = block_exponent(amax);
+    for (int i = 0; i < n; i++) {
+        double t = ldexp(fabs(v[i]), -e);   /* exact: scaling by a power of two */
+        int code = nearest_magnitude_code(t);
+        if (signbit(v[i]))
+            code |= 8;
+        codes4[i] = (uint8_t)code;
+    }
+    return e + 127;
+}
+
+/* Codes are packed two per byte along a row: element 2i in bits 3:0,
+ * element 2i+1 in bits 7:4. */
+static void put_code(uint8_t *codes, int64_t cols, int64_t r, int64_t c, int code)
+{
+    uint8_t *p = &codes[r * (cols / 2) + c / 2];
+    if (c & 1)
+        *p = (uint8_t)((*p & 0x0F) | (code << 4));
+    else
+        *p = (uint8_t)((*p & 0xF0) | code);
+}
+
+static int get_code(const uint8_t *codes, int64_t cols, int64_t r, int64_t c)
+{
+    uint8_t b = codes[r * (cols / 2) + c / 2];
+    return (c & 1) ? (b >> 4) : (b & 0x0F);
+}
+
+/*
+ * Quantize a bf16 matrix src[rows, cols] (row-major).
+ *   block_rows == 1 : 1x32 blocks along each row; scales[rows, cols/32]
+ *   block_rows == 32: 32x32 tiles; scales[rows/32, cols/32]
+ * codes[rows, cols/2] packed as described at put_code.
+ * Returns 0, or -1 for unsupported arguments.
+ */
+int fto_quantize(const uint16_t *src, int64_t rows, int64_t cols, int block_rows,
+                 uint8_t *codes, uint8_t *scales)
+{
+    if (cols % 32 != 0 || rows < 0 || (block_rows != 1 && block_rows != 32))
+        return -1;
+    if (block_rows == 32 && rows % 32 != 0)
+        return -1;
+    int64_t nbr = rows / block_rows, nbc = cols / 32;
+#pragma omp parallel for schedule(static)
+    for (int64_t br = 0; br < nbr; br++) {
+        double v[1024];
+        uint8_t c4[1024];
+        for (int64_t bc = 0; bc < nbc; bc++) {
+            int n = 0;
+            for (int i = 0; i < block_rows; i++)
+                for (int j = 0; j < 32; j++)
+                    v[n++] = bf16_value(src[(br * block_rows + i) * cols + bc * 32 + j]);
+            scales[br * nbc + bc] = (uint8_t)quantize_block(v, n, c4);
+            n = 0;
+            for (int i = 0; i < block_rows; i++)
+                for (int j = 0; j < 32; j++)
+                    put_code(codes, cols, br * block_rows + i, bc * 32 + j, c4[n++]);
+        }
+    }
+    return 0;
+}
+
+/* Dequantize codes/scales (layout as fto_quantize) into out[rows, cols]. */
+int fto_dequantize(const uint8_t *codes, const uint8_t *scales, int64_t rows, int64_t cols,
+                   int block_rows, double *out)
+{
+    if (cols % 32 != 0 || (block_rows != 1 && block_rows != 32))
+        return -1;
+    if (block_rows == 32 && rows % 32 != 0)
+        return -1;
+    int64_t nbc = cols / 32;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; r++)
+        for (int64_t c = 0; c < cols; c++) {
+            int s = scales[(r / block_rows) * nbc + c / 32];
+            out[r * cols + c] = fto_e2m1_value(get_code(codes, cols, r, c)) * fto_e8m0_value(s);
+        }
+    return 0;
+}
+
+/* ------------------------------------------------------- low-rank products */
+
+/*
+ * Down-projection of a bf16 matrix src[rows, cols]:
+ *   layout 0: proj is [cols, R] and out = src . proj      (X . [L1 | A])
+ *   layout 1: proj is [R, cols] and out = src . proj^T    (G . [L2 ; B]^T)
+ * out[rows, R] in fp64; out_abs (optional) = |src| . |proj| for error scales.
+ */
+int fto_proj(const uint16_t *src, int64_t rows, int64_t cols, const uint16_t *proj, int64_t R,
+             int layout, double *out, double *out_abs)
+{
+    if (layout != 0 && layout != 1)
+        return -1;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; r++)
+        for (int64_t j = 0; j < R; j++) {
+            double s = 0.0, a = 0.0;
+            for (int64_t c = 0; c < cols; c++) {
+                double x = bf16_value(src[r * cols + c]);
+                double p = bf16_value(layout == 0 ? proj[c * R + j] : proj[j * cols + c]);
+                s += x * p;
+                a += fabs(x) * fabs(p);
+            }
+            out[r * R + j] = s;
+            if (out_abs)
+                out_abs[r * R + j] = a;
+        }
+    return 0;
+}
+
+/* --------------------------------------------------------------- forward */
+
+/*
+ * Triple-branch forward, Eq. (2), with the weight in nn.Linear orientation
+ * W[N, K] (the paper's R is W^T):
+ *   y[m,n] = sum_k DQ(xq)[m,k] DQ(wq)[n,k] + sum_j P[m,j] U[j,n] + bias[n]
+ * xq/xs: X codes [M, K/2] and 1x32 scales [M, K/32]
+ * wq/ws: W codes [N, K/2] and 32x32 scales [N/32, K/32]
+ * P[M, R]: the down-projection X . [L1 | A]; U[R, N] = [L2 ; B] (bf16)
+ * Pabs[M, R] (optional): |X| . |[L1 | A]|, used only for s; if NULL, |P| is used.
+ * bias[N] (bf16, optional).  y and s (optional) are [M, N].
+ */
+int fto_linear_fwd(const uint8_t *xq, const uint8_t *xs, int64_t M, int64_t K,
+                   const uint8_t *wq, const uint8_t *ws, int64_t N,
+                   const double *P, const double *Pabs, int64_t R, const uint16_t *U,
+                   const uint16_t *bias, double *y, double *s)
+{
+    if (K % 32 != 0 || N % 32 != 0)
+        return -1;
+    double *xd = malloc(sizeof(double) * (size_t)(M * K + 1));
+    double *wd = malloc(sizeof(double) * (size_t)(N * K + 1));
+    if (!xd || !wd) {
+        free(xd);
+        free(wd);
+        return -2;
+    }
+    fto_dequantize(xq, xs, M, K, 1, xd);
+    fto_dequantize(wq, ws, N, K, 32, wd);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t m = 0; m < M; m++)
+        for (int64_t n = 0; n < N; n++) {
+            double acc = 0.0, mag = 0.0;
+            for (int64_t k = 0; k < K; k++) {
+                double t = xd[m * K + k] * wd[n * K + k];
+                acc += t;
+                mag += fabs(t);
+            }
+            for (int64_t j = 0; j < R; j++) {
+                double u = bf16_value(U[j * N + n]);
+                acc += P[m * R + j] * u;
+                mag += (Pabs ? Pabs[m * R + j] : fabs(P[m * R + j])) * fabs(u);
+            }
+            if (bias) {
+                double b = bf16_value(bias[n]);
+                acc += b;
+                mag += fabs(b);
+            }
+            y[m * N + n] = acc;
+            if (s)
+                s[m * N + n] = mag;
+        }
+    free(xd);
+    free(wd);
+    return 0;
+}
+
+/* ------------------------------------------------------- input gradient */
+
+/*
+ * Input gradient, Eq. (3), reusing the forward's weight codes and 32x32 scales
+ * read in transposed order (Sec. 3.2):
+ *   dx[m,k] = sum_n DQ(gq)[m,n] DQ(wq)[n,k] + sum_j Qp[m,j] D[k,j]
+ * gq/gs: G codes [M, N/2] and 1x32 scales [M, N/32]
+ * Qp[M, R]: G . [L2 ; B]^T;  D[K, R] = [L1 | A] (bf16)
+ * Qpabs (optional): |G| . |[L2 ; B]|^T for s; if NULL, |Qp| is used.
+ */
+int fto_linear_bwd_input(const uint8_t *gq, const uint8_t *gs, int64_t M, int64_t N,
+                         const uint8_t *wq, const uint8_t *ws, int64_t K,
+                         const double *Qp, const double *Qpabs, int64_t R, const uint16_t *D,
+                         double *dx, double *s)
+{
+    if (K % 32 != 0 || N % 32 != 0)
+        return -1;
+    double *gd = malloc(sizeof(double) * (size_t)(M * N + 1));
+    double *wd = malloc(sizeof(double) * (size_t)(N * K + 1));
+    if (!gd || !wd) {
+        free(gd);
+        free(wd);
+        return -2;
+    }
+    fto_dequantize(gq, gs, M, N, 1, gd);
+    fto_dequantize(wq, ws, N, K, 32, wd);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t m = 0; m < M; m++)
+        for (int64_t k = 0; k < K; k++) {
+            double acc = 0.0, mag = 0.0;
+            for (int64_t n = 0; n < N; n++) {
+                double t = gd[m * N + n] * wd[n * K + k];
+                acc += t;
+                mag += fabs(t);
+            }
+            for (int64_t j = 0; j < R; j++) {
+                double d = bf16_value(D[k * R + j]);
+                acc += Qp[m * R + j] * d;
+                mag += (Qpabs ? Qpabs[m * R + j] : fabs(Qp[m * R + j])) * fabs(d);
+            }
+            dx[m * K + k] = acc;
+            if (s)
+                s[m * K + k] = mag;
+        }
+    free(gd);
+    free(wd);
+    return 0;
+}
+
+/* ------------------------------------------------------ adapter gradients */
+
+/*
+ * Adapter weight gradients (Sec. 3.2):
+ *   dA[k,j] = sum_m X[m,k] (G B^T)[m,j]     dA = X^T (G B^T),  [K, r]
+ *   dB[j,n] = sum_m (X A)[m,j] G[m,n]       dB = (X A)^T G,    [r, N]
+ * x[M, K] and g[M, N] are bf16; xa[M, ld] holds X A in columns [0, r) and
+ * gbt[M, ld] holds G B^T in columns [0, r) (fp64).  sA, sB (optional) receive
+ * the matching sums of |terms|.
+ */
+int fto_lora_grads(const uint16_t *x, int64_t M, int64_t K, const uint16_t *g, int64_t N,
+                   const double *xa, const double *gbt, int64_t ld, int64_t r,
+                   double *dA, double *dB, double *sA, double *sB)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t k = 0; k < K; k++)
+        for (int64_t j = 0; j < r; j++) {
+            double acc = 0.0, mag = 0.0;
+            for (int64_t m = 0; m < M; m++) {
+                double t = bf16_value(x[m * K + k]) * gbt[m * ld + j];
+                acc += t;
+                mag += fabs(t);
+            }
+            dA[k * r + j] = acc;
+            if (sA)
+                sA[k * r + j] = mag;
+        }
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < r; j++)
+        for (int64_t n = 0; n < N; n++) {
+            double acc = 0.0, mag = 0.0;
+            for (int64_t m = 0; m < M; m++) {
+                double t = xa[m * ld + j] * bf16_value(g[m * N + n]);
+                acc += t;
+                mag += fabs(t);
+            }
+            dB[j * N + n] = acc;
+            if (sB)
+                sB[j * N + n] = mag;
+        }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ GELU */
+
+/* GELU, tanh form: 0.5 z (1 + tanh(c (z + 0.044715 z^3))), c = sqrt(2/pi). */
+double fto_gelu(double z)
+{
+    const double c = sqrt(2.0 / M_PI);
+    return 0.5 * z * (1.0 + tanh(c * (z + 0.044715 * z * z * z)));
+}
+
+/* d/dz of fto_gelu. */
+double fto_gelu_grad(double z)
+{
+    const double c = sqrt(2.0 / M_PI);
+    double u = c * (z + 0.044715 * z * z * z);
+    double th = tanh(u);
+    double du = c * (1.0 + 3.0 * 0.044715 * z * z);
+    return 0.5 * (1.0 + th) + 0.5 * z * (1.0 - th * th) * du;
+}
+
+/* Elementwise GELU / GELU' over n doubles (convenience for tests). */
+void fto_gelu_vec(const double *z, int64_t n, double *out, int derivative)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; i++)
+        out[i] = derivative ? fto_gelu_grad(z[i]) : fto_gelu(z[i]);
+}

@@ -1,0 +1,198 @@
+"""Pins of the oracle's GEMMs, low-rank branches and gradients (CPU only).
+
+  * exact rational arithmetic (fractions) on small dyadic problems must equal
+    the fp64 oracle exactly: decoding, index order, scale indexing and the
+    transposed weight read are checked with no rounding slack;
+  * numpy fp64 products on the dequantized operands (a library routine);
+  * the straight-through special case: with X and dY already on the MXFP4
+    grid, Eq. (2), Eq. (3) and the adapter gradients (Sec. 3.2) must equal
+    torch autograd of Y = X (W^T + L1 L2 + A B) + b in float64;
+  * closed-form points of GELU and a finite-difference check of its derivative.
+"""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import quant_exact, ref
+from paper_2607_05711_amd.gen import bf16_bits_to_f32, f32_to_bf16_bits
+from tests._helpers import f64, on_grid_rows, random_rows
+
+E2M1 = [Fraction(0), Fraction(1, 2), Fraction(1), Fraction(3, 2), Fraction(2), Fraction(3), Fraction(4), Fraction(6)]
+
+
+def frac_code(code, scale):
+    v = E2M1[code & 7] * (Fraction(2) ** (scale - 127))
+    return -v if code & 8 else v
+
+
+def frac_bf16(bits):
+    mag, sign = quant_exact.bf16_fraction(int(bits))
+    return -mag if sign else mag
+
+
+def unpack(q):
+    return np.stack([q & 0xF, q >> 4], axis=-1).reshape(q.shape[0], -1)
+
+
+def random_codes(rng, rows, cols, block_rows, lo=120, hi=134):
+    q = rng.integers(0, 256, (rows, cols // 2)).astype(np.uint8)
+    s = rng.integers(lo, hi, (rows // block_rows, cols // 32)).astype(np.uint8)
+    return q, s
+
+
+def test_fwd_exact_rational():
+    rng = np.random.default_rng(0)
+    M, K, N, R = 5, 96, 64, 16
+    xq, xs = random_codes(rng, M, K, 1)
+    wq, ws = random_codes(rng, N, K, 32)
+    P = rng.integers(-64, 64, (M, R)) / 8.0          # dyadic, exact in fp64
+    U = f32_to_bf16_bits((rng.integers(-64, 64, (R, N)) / 16.0).astype(np.float32))
+    bias = f32_to_bf16_bits((rng.integers(-64, 64, N) / 32.0).astype(np.float32))
+    y, s = ref.linear_fwd(xq, xs, wq, ws, K, P, U, bias)
+    xc, wc = unpack(xq), unpack(wq)
+    for m in range(M):
+        for n in range(N):
+            acc = Fraction(0)
+            mag = Fraction(0)
+            for k in range(K):
+                t = frac_code(int(xc[m, k]), int(xs[m, k // 32])) * frac_code(int(wc[n, k]), int(ws[n // 32, k // 32]))
+                acc += t
+                mag += abs(t)
+            for j in range(R):
+                t = Fraction(P[m, j]) * frac_bf16(U[j, n])
+                acc += t
+                mag += abs(t)
+            acc += frac_bf16(bias[n])
+            mag += abs(frac_bf16(bias[n]))
+            assert Fraction(y[m, n]) == acc, (m, n)
+            assert Fraction(s[m, n]) == mag, (m, n)
+
+
+def test_bwd_exact_rational():
+    rng = np.random.default_rng(1)
+    M, N, K, R = 4, 96, 64, 16
+    gq, gs = random_codes(rng, M, N, 1)
+    wq, ws = random_codes(rng, N, K, 32)
+    Qp = rng.integers(-64, 64, (M, R)) / 8.0
+    D = f32_to_bf16_bits((rng.integers(-64, 64, (K, R)) / 16.0).astype(np.float32))
+    dx, _ = ref.linear_bwd_input(gq, gs, wq, ws, K, Qp, D)
+    gc, wc = unpack(gq), unpack(wq)
+    for m in range(M):
+        for k in range(K):
+            acc = Fraction(0)
+            for n in range(N):
+                acc += frac_code(int(gc[m, n]), int(gs[m, n // 32])) * frac_code(int(wc[n, k]), int(ws[n // 32, k // 32]))
+            for j in range(R):
+                acc += Fraction(Qp[m, j]) * frac_bf16(D[k, j])
+            assert Fraction(dx[m, k]) == acc, (m, k)
+
+
+def test_proj_and_lora_exact_rational():
+    rng = np.random.default_rng(2)
+    M, K, N, r = 6, 64, 32, 4
+    x = f32_to_bf16_bits((rng.integers(-32, 32, (M, K)) / 4.0).astype(np.float32))
+    d = f32_to_bf16_bits((rng.integers(-32, 32, (K, r)) / 8.0).astype(np.float32))
+    u = f32_to_bf16_bits((rng.integers(-32, 32, (r, N)) / 8.0).astype(np.float32))
+    g = f32_to_bf16_bits((rng.integers(-32, 32, (M, N)) / 4.0).astype(np.float32))
+    p, pabs = ref.proj(x, d, 0)
+    qp, _ = ref.proj(g, u, 1)
+    for i in range(M):
+        for j in range(r):
+            want = sum(frac_bf16(x[i, k]) * frac_bf16(d[k, j]) for k in range(K))
+            assert Fraction(p[i, j]) == want
+            assert Fraction(pabs[i, j]) == sum(abs(frac_bf16(x[i, k]) * frac_bf16(d[k, j])) for k in range(K))
+            assert Fraction(qp[i, j]) == sum(frac_bf16(g[i, n]) * frac_bf16(u[j, n]) for n in range(N))
+    dA, dB, _, _ = ref.lora_grads(x, g, p, qp)
+    for k in range(K):
+        for j in range(r):
+            assert Fraction(dA[k, j]) == sum(frac_bf16(x[m, k]) * Fraction(qp[m, j]) for m in range(M))
+    for j in range(r):
+        for n in range(N):
+            assert Fraction(dB[j, n]) == sum(Fraction(p[m, j]) * frac_bf16(g[m, n]) for m in range(M))
+
+
+def test_fwd_bwd_against_numpy():
+    rng = np.random.default_rng(3)
+    M, K, N, R = 70, 320, 192, 32
+    x = random_rows("outliers", M, K, seed=1)
+    w = random_rows("normal", N, K, seed=2)
+    g = random_rows("student_t", M, N, seed=3)
+    D = f32_to_bf16_bits((0.05 * rng.standard_normal((K, R))).astype(np.float32))
+    U = f32_to_bf16_bits((0.05 * rng.standard_normal((R, N))).astype(np.float32))
+    bias = f32_to_bf16_bits((0.1 * rng.standard_normal(N)).astype(np.float32))
+    xq, xs = ref.quantize(x, 1)
+    wq, ws = ref.quantize(w, 32)
+    gq, gs = ref.quantize(g, 1)
+    P, Pabs = ref.proj(x, D, 0)
+    Qp, Qpabs = ref.proj(g, U, 1)
+    y, s = ref.linear_fwd(xq, xs, wq, ws, K, P, U, bias, Pabs=Pabs)
+    Xd, Wd, Gd = ref.dequantize(xq, xs, K, 1), ref.dequantize(wq, ws, K, 32), ref.dequantize(gq, gs, N, 1)
+    y_np = Xd @ Wd.T + f64(x) @ f64(D) @ f64(U) + f64(bias)
+    assert np.all(np.abs(y - y_np) <= 1e-12 * s)
+    s_np = np.abs(Xd) @ np.abs(Wd).T + (np.abs(f64(x)) @ np.abs(f64(D))) @ np.abs(f64(U)) + np.abs(f64(bias))
+    assert np.allclose(s, s_np, rtol=1e-12)
+    dx, sdx = ref.linear_bwd_input(gq, gs, wq, ws, K, Qp, D, Qpabs=Qpabs)
+    dx_np = Gd @ Wd + f64(g) @ f64(U).T @ f64(D).T
+    assert np.all(np.abs(dx - dx_np) <= 1e-12 * sdx)
+
+
+def test_ste_special_case_matches_autograd():
+    """X and dY on the MXFP4 grid: the oracle's forward, input gradient and
+    adapter gradients equal autograd of the unquantized three-branch layer."""
+    rng = np.random.default_rng(4)
+    M, K, N, r, rs = 64, 256, 160, 8, 8
+    x = on_grid_rows(M, K, seed=5)
+    g = on_grid_rows(M, N, seed=6, e_lo=-14, e_hi=-10)
+    w = random_rows("normal", N, K, seed=7)
+    wq, ws = ref.quantize(w, 32)
+    Wd = ref.dequantize(wq, ws, K, 32)
+    L1 = f32_to_bf16_bits((0.02 * rng.standard_normal((K, rs))).astype(np.float32))
+    L2 = f32_to_bf16_bits((0.02 * rng.standard_normal((rs, N))).astype(np.float32))
+    A = f32_to_bf16_bits((0.01 * rng.standard_normal((K, r))).astype(np.float32))
+    B = f32_to_bf16_bits((0.01 * rng.standard_normal((r, N))).astype(np.float32))
+    bias = f32_to_bf16_bits((0.02 * rng.standard_normal(N)).astype(np.float32))
+    D = np.ascontiguousarray(np.concatenate([L1, A], 1))
+    U = np.ascontiguousarray(np.concatenate([L2, B], 0))
+
+    xq, xs = ref.quantize(x, 1)
+    gq, gs = ref.quantize(g, 1)
+    P, _ = ref.proj(x, D, 0)
+    Qp, _ = ref.proj(g, U, 1)
+    y, s = ref.linear_fwd(xq, xs, wq, ws, K, P, U, bias)
+    dx, sdx = ref.linear_bwd_input(gq, gs, wq, ws, K, Qp, D)
+    dA, dB, sA, sB = ref.lora_grads(x, g, P[:, rs:], Qp[:, rs:])
+
+    T = lambda a: torch.tensor(a, dtype=torch.float64)
+    X = T(f64(x)).requires_grad_(True)
+    tA = T(f64(A)).requires_grad_(True)
+    tB = T(f64(B)).requires_grad_(True)
+    Y = X @ T(Wd).T + X @ T(f64(L1)) @ T(f64(L2)) + X @ tA @ tB + T(f64(bias))
+    Y.backward(T(f64(g)))
+    assert np.all(np.abs(y - Y.detach().numpy()) <= 1e-12 * s)
+    assert np.all(np.abs(dx - X.grad.numpy()) <= 1e-12 * sdx)
+    assert np.all(np.abs(dA - tA.grad.numpy()) <= 1e-12 * sA)
+    assert np.all(np.abs(dB - tB.grad.numpy()) <= 1e-12 * sB)
+
+
+def test_gelu_closed_forms():
+    z = np.array([0.0, 50.0, -50.0, 1.0, -1.0, 3.0])
+    gl = ref.gelu(z)
+    gd = ref.gelu(z, derivative=True)
+    assert gl[0] == 0.0 and gd[0] == 0.5
+    assert gl[1] == 50.0 and gd[1] == 1.0
+    assert gl[2] == 0.0 and abs(gd[2]) < 1e-300
+    # 0.5 (1 + tanh u) = sigmoid(2u)
+    c = np.sqrt(2 / np.pi)
+    u = c * (z + 0.044715 * z ** 3)
+    with np.errstate(over="ignore"):
+        alt = z / (1.0 + np.exp(-2.0 * u))
+    assert np.allclose(gl, alt, rtol=1e-14, atol=1e-300)
+
+
+def test_gelu_derivative_finite_difference():
+    z = np.linspace(-6, 6, 241)
+    h = 1e-6
+    fd = (ref.gelu(z + h) - ref.gelu(z - h)) / (2 * h)
+    assert np.allclose(ref.gelu(z, derivative=True), fd, rtol=1e-7, atol=1e-8)
