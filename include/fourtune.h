@@ -1,0 +1,166 @@
+/*
+ * fourtune.h -- C ABI of the MI355X (gfx950) W4A4G4 triple-branch linear layer.
+ *
+ * Method: FourTune (arXiv 2607.05711), Section 3.  One linear layer carries
+ *   (1) a frozen 4-bit backbone weight W, used through 4-bit GEMMs,
+ *   (2) a frozen low-rank "numerical stabilizer" L1 L2 in bf16, and
+ *   (3) a trainable low-rank adapter A B in bf16,
+ * forward  (Eq. 2):  Y  = Q(X) Q(W)^T + X L1 L2 + X A B (+ bias)
+ * backward (Eq. 3):  dX = Q(G) Q(W)   + G (L1 L2)^T + G (A B)^T,   G = dL/dY
+ * adapter gradients (Sec. 3.2):  dB = (X A)^T G,  dA = X^T (G B^T).
+ * The two low-rank branches share their input, so the library concatenates
+ * them: D = [L1 | A] is [K, R] ("down") and U = [L2 ; B] is [R, N] ("up"),
+ * R = r_s + r, stabilizer first (Sec. 3.3, LoRA fusion).
+ *
+ * Number format (paper: NVFP4, Sec. 3.1; read here as the OCP Microscaling
+ * MXFP4 format the paper cites in Sec. 2.3, which gfx950's block-scaled MFMA
+ * consumes): 4-bit E2M1 codes, two per byte (element 2i in bits 3:0, element
+ * 2i+1 in bits 7:4), with one E8M0 power-of-two scale per block.
+ *   - X and G: 1x32 blocks along the GEMM reduction axis (K for X, N for G).
+ *   - W: 32x32 tiles, scales [N/32, K/32], so the backward GEMM reads the
+ *     same codes and scales in transposed order (Sec. 3.2, block-wise
+ *     quantization) with no re-quantization.
+ * Block rule: e = floor(log2(max|v|)) - 2 clamped to [-127, 127] (a zero block
+ * gets e = -127), scale byte = e + 127; each element becomes the nearest
+ * E2M1 value of v / 2^e, ties to the even code, saturating at 6, with the
+ * input's sign bit (also for -0).
+ *
+ * Conventions for every call:
+ *   - All tensors are dense row-major device buffers owned by the caller.  The
+ *     library never allocates, frees or synchronizes; work is enqueued on
+ *     `stream` (a hipStream_t; NULL = the default stream) and runs
+ *     asynchronously.
+ *   - bf16 tensors are passed as `const void*` holding IEEE bfloat16 values.
+ *   - Every tensor pointer must be 16-byte aligned, except `scales`, `xs`,
+ *     `gs`, `ws` (any alignment).
+ *   - Arguments are validated before anything is enqueued; on error nothing is
+ *     launched and the return value says why (ft_last_error() has details).
+ *   - FT_ERR_HIP means a launch was rejected by the HIP runtime; earlier
+ *     kernels of the same call may already be enqueued.
+ *   - Inputs are assumed finite.  Calls on the same stream are ordered; calls
+ *     that write the same buffers from different streams race.
+ */
+#ifndef FOURTUNE_H
+#define FOURTUNE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *hipStream_t;
+
+typedef enum ft_status {
+    FT_OK = 0,
+    FT_ERR_NULL = 1,         /* a required pointer is NULL */
+    FT_ERR_SHAPE = 2,        /* a size is negative, too large, or not a multiple of 32 where required */
+    FT_ERR_ALIGN = 3,        /* a tensor pointer is not 16-byte aligned */
+    FT_ERR_UNSUPPORTED = 4,  /* valid but unsupported option (e.g. R > 128, R % 16 != 0) */
+    FT_ERR_HIP = 5           /* the HIP runtime rejected a launch */
+} ft_status;
+
+typedef enum ft_dtype { FT_BF16 = 0, FT_F32 = 1 } ft_dtype;
+
+typedef enum ft_proj_layout {
+    FT_PROJ_COLS_BY_R = 0,   /* proj is [cols, R]; proj_out = src . proj   (forward: D) */
+    FT_PROJ_R_BY_COLS = 1    /* proj is [R, cols]; proj_out = src . proj^T (backward: U) */
+} ft_proj_layout;
+
+/*
+ * Block-wise MXFP4 quantization of a bf16 matrix, optionally fused with the
+ * low-rank down-projection of the same input (Sec. 3.3: the three branches
+ * share their input, so one pass reads it once).
+ *
+ *   src        bf16 [rows, cols]; cols % 32 == 0.
+ *   block_rows 1  -> 1x32 blocks along each row (activations X, gradients G);
+ *                    scales is [rows, cols/32].
+ *              32 -> 32x32 tiles (the frozen weight, prepared offline);
+ *                    rows % 32 == 0; scales is [rows/32, cols/32].
+ *   codes      uint8 [rows, cols/2], packed E2M1 (see above).
+ *   scales     uint8 E8M0 codes, layout as above.
+ *   proj       bf16, NULL for none.  layout FT_PROJ_COLS_BY_R: [cols, R]
+ *              (forward, D = [L1|A]); FT_PROJ_R_BY_COLS: [R, cols] (backward,
+ *              U = [L2;B]).  Only with block_rows == 1.
+ *   R          0 when proj is NULL; else 16 <= R <= 128 and R % 16 == 0.
+ *   proj_out   fp32 [rows, R] = src . proj (or src . proj^T), products of the
+ *              unquantized bf16 inputs with fp32 accumulation.  Partial sums
+ *              over column chunks are combined with atomic adds, so the last
+ *              bit may vary between runs.
+ * rows == 0 is a no-op.  rows < 2^31, cols < 2^31.
+ */
+ft_status ft_quantize_blockwise(const void *src, int64_t rows, int64_t cols, int32_t block_rows,
+                                uint8_t *codes, uint8_t *scales,
+                                const void *proj, int32_t R, ft_proj_layout proj_layout,
+                                float *proj_out, hipStream_t stream);
+
+/*
+ * Forward of the triple-branch linear, Eq. (2), in nn.Linear orientation:
+ *   y[m,n] = sum_k DQ(xq)[m,k] DQ(wq)[n,k] + sum_j P[m,j] U[j,n] + bias[n]
+ * The 4-bit product runs on block-scaled FP4 MFMA with fp32 accumulation; the
+ * low-rank up-projection and the bias are added in the same kernel's
+ * epilogue (Sec. 3.3).  P is split as P = hi + lo (two bf16 terms) so the
+ * up-projection keeps ~16 significant bits of P.
+ *
+ *   xq, xs   X codes [M, K/2] and 1x32 scales [M, K/32] (ft_quantize_blockwise).
+ *   wq, ws   W codes [N, K/2] and 32x32 scales [N/32, K/32].
+ *   M >= 0;  K, N multiples of 32.
+ *   P        fp32 [M, R] = X . D (from ft_quantize_blockwise); NULL iff R == 0.
+ *   U        bf16 [R, N] = [L2 ; B]; NULL iff R == 0.  R % 16 == 0, R <= 128.
+ *   bias     bf16 [N] or NULL.
+ *   y        [M, N], bf16 (round to nearest even) or fp32.
+ */
+ft_status ft_linear_fwd(const uint8_t *xq, const uint8_t *xs, int64_t M, int64_t K,
+                        const uint8_t *wq, const uint8_t *ws, int64_t N,
+                        const float *P, int32_t R, const void *U,
+                        const void *bias, void *y, ft_dtype y_dtype, hipStream_t stream);
+
+/*
+ * Input gradient of the triple-branch linear, Eq. (3):
+ *   dx[m,k] = sum_n DQ(gq)[m,n] DQ(wq)[n,k] + sum_j Qp[m,j] D[k,j]
+ * The weight codes and 32x32 scales are the forward's, read in transposed
+ * order inside the kernel (Sec. 3.2); nothing is re-quantized.
+ *
+ *   gq, gs   G codes [M, N/2] and 1x32 scales [M, N/32].
+ *   wq, ws   W codes [N, K/2] and 32x32 scales [N/32, K/32].
+ *   Qp       fp32 [M, R] = G . U^T (from ft_quantize_blockwise); NULL iff R == 0.
+ *   D        bf16 [K, R] = [L1 | A]; NULL iff R == 0.
+ *   dx       [M, K], bf16 or fp32.
+ */
+ft_status ft_linear_bwd_input(const uint8_t *gq, const uint8_t *gs, int64_t M, int64_t N,
+                              const uint8_t *wq, const uint8_t *ws, int64_t K,
+                              const float *Qp, int32_t R, const void *D,
+                              void *dx, ft_dtype dx_dtype, hipStream_t stream);
+
+/*
+ * Adapter weight gradients (Sec. 3.2):
+ *   dA[k,j] = sum_m X[m,k] dyb[m,j]    (dA = X^T (G B^T))
+ *   dB[j,n] = sum_m xa[m,j] G[m,n]     (dB = (X A)^T G)
+ * X is the unquantized bf16 input saved by the forward pass.
+ *
+ *   x        bf16 [M, K];  dy: bf16 [M, N] (the incoming gradient G).
+ *   xa       fp32, row stride ld: columns [0, r) hold X A (pass P + r_s).
+ *   dyb      fp32, row stride ld: columns [0, r) hold G B^T (pass Qp + r_s).
+ *   ld       row stride of xa and dyb in elements (R); ld >= r, ld % 4 == 0.
+ *   r        1 <= r <= 128.
+ *   dA       fp32 [K, r];  dB: fp32 [r, N].
+ *   accumulate  0: overwrite dA and dB;  1: add into them.
+ * Sums over M are combined across workgroups with atomic adds (last-bit
+ * run-to-run variation).  K, N multiples of 32; M >= 0.
+ */
+ft_status ft_lora_grads(const void *x, int64_t M, int64_t K, const void *dy, int64_t N,
+                        const float *xa, const float *dyb, int64_t ld, int32_t r,
+                        float *dA, float *dB, int32_t accumulate, hipStream_t stream);
+
+/* Static description of a status code. */
+const char *ft_status_string(ft_status status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char *ft_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FOURTUNE_H */

@@ -34,6 +34,7 @@
  * Build:  gcc -O2 -fopenmp -shared -fPIC ft_oracle.c -o libft_oracle.so -lm
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -389,4 +390,10 @@ void fto_gelu_vec(const double *z, int64_t n, double *out, int derivative)
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; i++)
         out[i] = derivative ? fto_gelu_grad(z[i]) : fto_gelu(z[i]);
+}
+
+/* Number of OpenMP threads the oracle's parallel loops use. */
+int fto_num_threads(void)
+{
+    return omp_get_max_threads();
 }

@@ -53,6 +53,8 @@ def lib():
         L.fto_gelu_grad.restype = ctypes.c_double
         L.fto_gelu_grad.argtypes = [ctypes.c_double]
         L.fto_gelu_vec.argtypes = [_ptr, _c_i64, _ptr, ctypes.c_int]
+        L.fto_num_threads.restype = ctypes.c_int
+        L.fto_num_threads.argtypes = []
         for f in ("fto_quantize", "fto_dequantize", "fto_proj", "fto_linear_fwd",
                   "fto_linear_bwd_input", "fto_lora_grads"):
             getattr(L, f).restype = ctypes.c_int
@@ -156,6 +158,10 @@ def lora_grads(x_bits, g_bits, xa, gbt, want_s=True):
     sB = np.zeros((r, N)) if want_s else None
     lib().fto_lora_grads(_p(x), M, K, _p(g), N, _p(xa), _p(gbt), r, r, _p(dA), _p(dB), _p(sA), _p(sB))
     return dA, dB, sA, sB
+
+
+def num_threads():
+    return int(lib().fto_num_threads())
 
 
 def gelu(z, derivative=False):

@@ -1,0 +1,219 @@
+"""Python binding of libfourtune (ctypes): argument marshalling only.
+
+Each function has the name of the C entry point it calls (include/fourtune.h),
+checks dtypes, devices and shapes of torch tensors, allocates missing outputs
+with torch (device memory only) and enqueues the library call on the current
+HIP stream.  All arithmetic runs in the library's gfx950 kernels; there is no
+fallback: if the shared library is not built, every call raises.
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfourtune.so")
+
+FT_OK, FT_ERR_NULL, FT_ERR_SHAPE, FT_ERR_ALIGN, FT_ERR_UNSUPPORTED, FT_ERR_HIP = range(6)
+FT_BF16, FT_F32 = 0, 1
+FT_PROJ_COLS_BY_R, FT_PROJ_R_BY_COLS = 0, 1
+
+EXPORTED = ("ft_quantize_blockwise", "ft_linear_fwd", "ft_linear_bwd_input", "ft_lora_grads",
+            "ft_status_string", "ft_last_error")
+
+
+class FourTuneError(RuntimeError):
+    def __init__(self, status, detail):
+        self.status = status
+        super().__init__("%s (status %d): %s" % (status_string(status), status, detail))
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+
+
+def load():
+    """Load libfourtune.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise FileNotFoundError(
+                "libfourtune.so is not built (expected at %s); run `python -m paper_2607_05711_amd.build` "
+                "or __graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        L.ft_quantize_blockwise.argtypes = [_P, _I64, _I64, _I32, _P, _P, _P, _I32, ctypes.c_int, _P, _P]
+        L.ft_linear_fwd.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P, _P, ctypes.c_int, _P]
+        L.ft_linear_bwd_input.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P, ctypes.c_int, _P]
+        L.ft_lora_grads.argtypes = [_P, _I64, _I64, _P, _I64, _P, _P, _I64, _I32, _P, _P, _I32, _P]
+        for f in ("ft_quantize_blockwise", "ft_linear_fwd", "ft_linear_bwd_input", "ft_lora_grads"):
+            getattr(L, f).restype = ctypes.c_int
+        L.ft_status_string.argtypes = [ctypes.c_int]
+        L.ft_status_string.restype = ctypes.c_char_p
+        L.ft_last_error.argtypes = []
+        L.ft_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(status):
+    return load().ft_status_string(int(status)).decode()
+
+
+def _check(status):
+    if status != FT_OK:
+        raise FourTuneError(status, load().ft_last_error().decode())
+
+
+def _ptr(t, offset_elems=0):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr() + offset_elems * t.element_size())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need(t, name, dtype, device=None, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if t.device.type != "cuda":
+        raise ValueError("%s must be on a GPU, got %s" % (name, t.device))
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError("%s must be %d-D, got shape %s" % (name, ndim, tuple(t.shape)))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return t
+
+
+def ft_quantize_blockwise(src, block_rows=1, proj=None, proj_layout=FT_PROJ_COLS_BY_R,
+                          codes=None, scales=None, proj_out=None):
+    """MXFP4-quantize bf16 src [rows, cols]; optionally fused down-projection.
+
+    Returns (codes uint8 [rows, cols/2], scales uint8, proj_out fp32 [rows, R] or None).
+    """
+    L = load()
+    _need(src, "src", torch.bfloat16, ndim=2)
+    dev = src.device
+    rows, cols = src.shape
+    if codes is None:
+        codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=dev)
+    if scales is None:
+        scales = torch.empty((rows // block_rows, cols // 32), dtype=torch.uint8, device=dev)
+    _need(codes, "codes", torch.uint8, dev)
+    _need(scales, "scales", torch.uint8, dev)
+    if codes.numel() * 2 != rows * cols or scales.numel() * 32 * block_rows != rows * cols:
+        raise ValueError("codes/scales size does not match src %s with block_rows %d" % (tuple(src.shape), block_rows))
+    R = 0
+    if proj is not None:
+        _need(proj, "proj", torch.bfloat16, dev, ndim=2)
+        R = proj.shape[1] if proj_layout == FT_PROJ_COLS_BY_R else proj.shape[0]
+        other = proj.shape[0] if proj_layout == FT_PROJ_COLS_BY_R else proj.shape[1]
+        if other != cols:
+            raise ValueError("proj shape %s does not match cols %d" % (tuple(proj.shape), cols))
+        if proj_out is None:
+            proj_out = torch.empty((rows, R), dtype=torch.float32, device=dev)
+        _need(proj_out, "proj_out", torch.float32, dev)
+        if proj_out.shape != (rows, R):
+            raise ValueError("proj_out must be [%d, %d]" % (rows, R))
+    else:
+        proj_out = None
+    _check(L.ft_quantize_blockwise(_ptr(src), rows, cols, block_rows, _ptr(codes), _ptr(scales),
+                                   _ptr(proj), R, proj_layout, _ptr(proj_out), _stream(dev)))
+    return codes, scales, proj_out
+
+
+def ft_linear_fwd(xq, xs, wq, ws, K, P=None, U=None, bias=None, out_dtype=torch.bfloat16, y=None):
+    """y[M, N] = DQ(xq) DQ(wq)^T + P U + bias (Eq. 2)."""
+    L = load()
+    dev = xq.device
+    _need(xq, "xq", torch.uint8, ndim=2)
+    _need(xs, "xs", torch.uint8, dev)
+    _need(wq, "wq", torch.uint8, dev, ndim=2)
+    _need(ws, "ws", torch.uint8, dev)
+    M, N = xq.shape[0], wq.shape[0]
+    if xq.shape[1] * 2 != K or wq.shape[1] * 2 != K or xs.numel() * 32 != M * K or ws.numel() * 1024 != N * K:
+        raise ValueError("operand shapes do not match K=%d" % K)
+    R = 0
+    if P is not None or U is not None:
+        _need(P, "P", torch.float32, dev, ndim=2)
+        _need(U, "U", torch.bfloat16, dev, ndim=2)
+        R = P.shape[1]
+        if P.shape[0] != M or U.shape != (R, N):
+            raise ValueError("P [M,R] / U [R,N] shapes mismatch")
+    if bias is not None:
+        _need(bias, "bias", torch.bfloat16, dev)
+        if bias.numel() != N:
+            raise ValueError("bias must have N elements")
+    if y is None:
+        y = torch.empty((M, N), dtype=out_dtype, device=dev)
+    if y.dtype not in (torch.bfloat16, torch.float32) or y.shape != (M, N):
+        raise ValueError("y must be bf16 or fp32 [M, N]")
+    _need(y, "y", y.dtype, dev)
+    _check(L.ft_linear_fwd(_ptr(xq), _ptr(xs), M, K, _ptr(wq), _ptr(ws), N, _ptr(P), R, _ptr(U), _ptr(bias),
+                           _ptr(y), FT_F32 if y.dtype == torch.float32 else FT_BF16, _stream(dev)))
+    return y
+
+
+def ft_linear_bwd_input(gq, gs, wq, ws, K, Qp=None, D=None, out_dtype=torch.bfloat16, dx=None):
+    """dx[M, K] = DQ(gq) DQ(wq) + Qp D^T (Eq. 3)."""
+    L = load()
+    dev = gq.device
+    _need(gq, "gq", torch.uint8, ndim=2)
+    _need(gs, "gs", torch.uint8, dev)
+    _need(wq, "wq", torch.uint8, dev, ndim=2)
+    _need(ws, "ws", torch.uint8, dev)
+    M, N = gq.shape[0], wq.shape[0]
+    if gq.shape[1] * 2 != N or wq.shape[1] * 2 != K or gs.numel() * 32 != M * N or ws.numel() * 1024 != N * K:
+        raise ValueError("operand shapes do not match N=%d K=%d" % (N, K))
+    R = 0
+    if Qp is not None or D is not None:
+        _need(Qp, "Qp", torch.float32, dev, ndim=2)
+        _need(D, "D", torch.bfloat16, dev, ndim=2)
+        R = Qp.shape[1]
+        if Qp.shape[0] != M or D.shape != (K, R):
+            raise ValueError("Qp [M,R] / D [K,R] shapes mismatch")
+    if dx is None:
+        dx = torch.empty((M, K), dtype=out_dtype, device=dev)
+    if dx.dtype not in (torch.bfloat16, torch.float32) or dx.shape != (M, K):
+        raise ValueError("dx must be bf16 or fp32 [M, K]")
+    _need(dx, "dx", dx.dtype, dev)
+    _check(L.ft_linear_bwd_input(_ptr(gq), _ptr(gs), M, N, _ptr(wq), _ptr(ws), K, _ptr(Qp), R, _ptr(D),
+                                 _ptr(dx), FT_F32 if dx.dtype == torch.float32 else FT_BF16, _stream(dev)))
+    return dx
+
+
+def ft_lora_grads(x, dy, xa, dyb, r, col0=0, dA=None, dB=None, accumulate=False):
+    """dA = x^T dyb[:, col0:col0+r] [K, r];  dB = xa[:, col0:col0+r]^T dy [r, N].
+
+    xa and dyb are contiguous fp32 [M, ld] (normally P and Qp, with the adapter
+    columns starting at col0 = r_s).
+    """
+    L = load()
+    dev = x.device
+    _need(x, "x", torch.bfloat16, ndim=2)
+    _need(dy, "dy", torch.bfloat16, dev, ndim=2)
+    _need(xa, "xa", torch.float32, dev, ndim=2)
+    _need(dyb, "dyb", torch.float32, dev, ndim=2)
+    M, K = x.shape
+    N = dy.shape[1]
+    ld = xa.shape[1]
+    if dy.shape[0] != M or xa.shape[0] != M or dyb.shape != xa.shape or col0 + r > ld:
+        raise ValueError("x [M,K], dy [M,N], xa/dyb [M,ld] shapes mismatch")
+    if dA is None:
+        dA = torch.empty((K, r), dtype=torch.float32, device=dev)
+    if dB is None:
+        dB = torch.empty((r, N), dtype=torch.float32, device=dev)
+    _need(dA, "dA", torch.float32, dev)
+    _need(dB, "dB", torch.float32, dev)
+    if dA.shape != (K, r) or dB.shape != (r, N):
+        raise ValueError("dA must be [K, r] and dB [r, N]")
+    _check(L.ft_lora_grads(_ptr(x), M, K, _ptr(dy), N, _ptr(xa, col0), _ptr(dyb, col0), ld, r,
+                           _ptr(dA), _ptr(dB), 1 if accumulate else 0, _stream(dev)))
+    return dA, dB

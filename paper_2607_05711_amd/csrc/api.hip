@@ -1,0 +1,151 @@
+// C ABI of libfourtune: argument validation, then kernel launches.
+// Nothing here allocates, frees or synchronizes.
+#include <cstdarg>
+#include <cstdio>
+
+#include "../../include/fourtune.h"
+#include "ft_kernels.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+ft_status fail(ft_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+ft_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return FT_OK;
+  return fail(FT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+constexpr int64_t kMaxDim = (int64_t)1 << 30;
+
+ft_status check_dim(const char* name, int64_t v, int64_t mult) {
+  if (v < 0 || v > kMaxDim) return fail(FT_ERR_SHAPE, "%s = %lld out of range [0, 2^30]", name, (long long)v);
+  if (mult > 1 && v % mult != 0)
+    return fail(FT_ERR_SHAPE, "%s = %lld is not a multiple of %lld", name, (long long)v, (long long)mult);
+  return FT_OK;
+}
+
+ft_status check_rank(int32_t R, const void* a, const void* b, const char* an, const char* bn) {
+  if (R == 0) {
+    if (a || b) return fail(FT_ERR_UNSUPPORTED, "R == 0 but %s/%s given", an, bn);
+    return FT_OK;
+  }
+  if (!a || !b) return fail(FT_ERR_NULL, "R = %d but %s or %s is NULL", R, an, bn);
+  if (R < 0 || R > 128 || R % 16 != 0) return fail(FT_ERR_UNSUPPORTED, "R = %d: need 16 <= R <= 128, R %% 16 == 0", R);
+  if (!aligned16(a) || !aligned16(b)) return fail(FT_ERR_ALIGN, "%s or %s not 16-byte aligned", an, bn);
+  return FT_OK;
+}
+
+#define FT_TRY(x)                   \
+  do {                              \
+    ft_status s_ = (x);             \
+    if (s_ != FT_OK) return s_;     \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* ft_status_string(ft_status s) {
+  switch (s) {
+    case FT_OK: return "ok";
+    case FT_ERR_NULL: return "null pointer";
+    case FT_ERR_SHAPE: return "invalid shape";
+    case FT_ERR_ALIGN: return "misaligned pointer";
+    case FT_ERR_UNSUPPORTED: return "unsupported argument";
+    case FT_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* ft_last_error(void) { return g_last_error; }
+
+ft_status ft_quantize_blockwise(const void* src, int64_t rows, int64_t cols, int32_t block_rows, uint8_t* codes,
+                                uint8_t* scales, const void* proj, int32_t R, ft_proj_layout proj_layout,
+                                float* proj_out, hipStream_t stream) {
+  g_last_error[0] = 0;
+  FT_TRY(check_dim("rows", rows, block_rows == 32 ? 32 : 1));
+  FT_TRY(check_dim("cols", cols, 32));
+  if (block_rows != 1 && block_rows != 32) return fail(FT_ERR_UNSUPPORTED, "block_rows = %d (1 or 32)", block_rows);
+  if (rows == 0 || cols == 0) return FT_OK;
+  if (!src || !codes || !scales) return fail(FT_ERR_NULL, "src, codes and scales are required");
+  if (!aligned16(src) || !aligned16(codes)) return fail(FT_ERR_ALIGN, "src or codes not 16-byte aligned");
+  if (proj_layout != FT_PROJ_COLS_BY_R && proj_layout != FT_PROJ_R_BY_COLS)
+    return fail(FT_ERR_UNSUPPORTED, "proj_layout = %d", (int)proj_layout);
+  FT_TRY(check_rank(R, proj, proj_out, "proj", "proj_out"));
+  if (block_rows == 32) {
+    if (R != 0) return fail(FT_ERR_UNSUPPORTED, "projection is only fused with 1x32 blocks");
+    return hip_status(ft::launch_quant_tiles((const uint16_t*)src, (int)rows, (int)cols, codes, scales, stream),
+                      "quantize 32x32");
+  }
+  return hip_status(ft::launch_quant_rows((const uint16_t*)src, (int)rows, (int)cols, codes, scales,
+                                          (const uint16_t*)proj, R, (int)proj_layout, proj_out, stream),
+                    "quantize 1x32");
+}
+
+ft_status ft_linear_fwd(const uint8_t* xq, const uint8_t* xs, int64_t M, int64_t K, const uint8_t* wq,
+                        const uint8_t* ws, int64_t N, const float* P, int32_t R, const void* U, const void* bias,
+                        void* y, ft_dtype y_dtype, hipStream_t stream) {
+  g_last_error[0] = 0;
+  FT_TRY(check_dim("M", M, 1));
+  FT_TRY(check_dim("K", K, 32));
+  FT_TRY(check_dim("N", N, 32));
+  if (y_dtype != FT_BF16 && y_dtype != FT_F32) return fail(FT_ERR_UNSUPPORTED, "y_dtype = %d", (int)y_dtype);
+  if (M == 0 || N == 0) return FT_OK;
+  if (K == 0) return fail(FT_ERR_SHAPE, "K == 0");
+  if (!xq || !xs || !wq || !ws || !y) return fail(FT_ERR_NULL, "xq, xs, wq, ws and y are required");
+  if (!aligned16(xq) || !aligned16(wq) || !aligned16(y) || (bias && !aligned16(bias)))
+    return fail(FT_ERR_ALIGN, "xq, wq, y, bias must be 16-byte aligned");
+  FT_TRY(check_rank(R, P, U, "P", "U"));
+  return hip_status(ft::launch_gemm_fp4(false, xq, xs, wq, ws, (int)M, (int)N, (int)K, P, R, (const uint16_t*)U,
+                                        (const uint16_t*)bias, y, y_dtype == FT_F32, stream),
+                    "linear fwd");
+}
+
+ft_status ft_linear_bwd_input(const uint8_t* gq, const uint8_t* gs, int64_t M, int64_t N, const uint8_t* wq,
+                              const uint8_t* ws, int64_t K, const float* Qp, int32_t R, const void* D, void* dx,
+                              ft_dtype dx_dtype, hipStream_t stream) {
+  g_last_error[0] = 0;
+  FT_TRY(check_dim("M", M, 1));
+  FT_TRY(check_dim("N", N, 32));
+  FT_TRY(check_dim("K", K, 32));
+  if (dx_dtype != FT_BF16 && dx_dtype != FT_F32) return fail(FT_ERR_UNSUPPORTED, "dx_dtype = %d", (int)dx_dtype);
+  if (M == 0 || K == 0) return FT_OK;
+  if (N == 0) return fail(FT_ERR_SHAPE, "N == 0");
+  if (!gq || !gs || !wq || !ws || !dx) return fail(FT_ERR_NULL, "gq, gs, wq, ws and dx are required");
+  if (!aligned16(gq) || !aligned16(wq) || !aligned16(dx)) return fail(FT_ERR_ALIGN, "gq, wq, dx must be 16-byte aligned");
+  FT_TRY(check_rank(R, Qp, D, "Qp", "D"));
+  return hip_status(ft::launch_gemm_fp4(true, gq, gs, wq, ws, (int)M, (int)N, (int)K, Qp, R, (const uint16_t*)D,
+                                        nullptr, dx, dx_dtype == FT_F32, stream),
+                    "linear bwd input");
+}
+
+ft_status ft_lora_grads(const void* x, int64_t M, int64_t K, const void* dy, int64_t N, const float* xa,
+                        const float* dyb, int64_t ld, int32_t r, float* dA, float* dB, int32_t accumulate,
+                        hipStream_t stream) {
+  g_last_error[0] = 0;
+  FT_TRY(check_dim("M", M, 1));
+  FT_TRY(check_dim("K", K, 32));
+  FT_TRY(check_dim("N", N, 32));
+  if (r < 1 || r > 128) return fail(FT_ERR_UNSUPPORTED, "r = %d: need 1 <= r <= 128", r);
+  if (ld < r || ld % 4 != 0 || ld > 4096) return fail(FT_ERR_SHAPE, "ld = %lld: need r <= ld <= 4096, ld %% 4 == 0", (long long)ld);
+  if (accumulate != 0 && accumulate != 1) return fail(FT_ERR_UNSUPPORTED, "accumulate = %d", accumulate);
+  if (!dA || !dB) return fail(FT_ERR_NULL, "dA and dB are required");
+  if (M > 0 && (!x || !dy || !xa || !dyb)) return fail(FT_ERR_NULL, "x, dy, xa and dyb are required");
+  if ((x && !aligned16(x)) || (dy && !aligned16(dy)) || !aligned16(dA) || !aligned16(dB))
+    return fail(FT_ERR_ALIGN, "x, dy, dA, dB must be 16-byte aligned");
+  return hip_status(ft::launch_lora_grads((const uint16_t*)x, (int)M, (int)K, (const uint16_t*)dy, (int)N, xa, dyb,
+                                          (int)ld, r, dA, dB, accumulate != 0, stream),
+                    "lora grads");
+}
+
+}  // extern "C"

@@ -1,0 +1,128 @@
+// Device-side helpers shared by the gfx950 kernels of libfourtune.
+//
+// Operand layouts of the CDNA4 matrix instructions used here (lane l of a
+// 64-wide wavefront):
+//   v_mfma_scale_f32_32x32x64_f8f6f4 (FP4 x FP4, E8M0 block scales):
+//     A: row l%32, reduction elements [32*(l/32), +32) as 16 packed bytes
+//        (element 2i in the low nibble of byte i), scale byte for that
+//        row/32-block chosen from a VGPR by op_sel;
+//     B: column l%32, same reduction split;
+//     C/D: column l%32, rows 8*(v/4) + 4*(l/32) + v%4 for v = 0..15.
+//   v_mfma_f32_32x32x16_bf16: A row l%32 / B column l%32, reduction
+//     elements [8*(l/32), +8); C/D as above.
+//   ds_read_b64_tr_b4: in each 16-lane group lane s supplies the address of
+//     16 nibbles (a row); lane c receives nibble c of rows 0..15, in order.
+//   ds_read_b64_tr_b16: in each 16-lane group, output lane i element j is
+//     halfword i%4 of source lane 4j + i/4.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ft {
+
+typedef int v2i __attribute__((ext_vector_type(2)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+#define FT_LDS __attribute__((address_space(3)))
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// Two-term bf16 split of an fp32 value: x ~= hi + lo with |x - hi - lo| <= 2^-16 |x|.
+__device__ __forceinline__ void split_bf16(float x, uint32_t& hi, uint32_t& lo) {
+  hi = f32_to_bf16_rne(x);
+  lo = f32_to_bf16_rne(x - bf16_to_f32(hi));
+}
+
+// E8M0 block scale from the largest |bf16| bit pattern of a block (sign
+// cleared): floor(log2 amax) - 2 + 127, clamped at 0.  A zero or subnormal
+// amax gives 0 (e = -127).
+__device__ __forceinline__ uint32_t e8m0_from_amax_bits(uint32_t amax_bits) {
+  int e = (int)((amax_bits >> 7) & 0xFF) - 2;
+  return e > 0 ? (uint32_t)e : 0u;
+}
+
+// 2^(code-127) as an fp32 (2^-127 is the subnormal 0x00400000).
+__device__ __forceinline__ float e8m0_to_f32(uint32_t code) {
+  return __uint_as_float(code ? (code << 23) : 0x00400000u);
+}
+
+// Quantize 32 bf16 values (16 dwords, element 2i in the low half of dword i)
+// to 16 bytes of packed E2M1 codes; returns the E8M0 code.  The conversion
+// instruction divides by the scale, rounds to nearest even and saturates,
+// copying the sign, which is the block rule of the library.
+__device__ __forceinline__ uint32_t quantize32(const uint32_t (&w)[16], uint32_t (&out)[4]) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < 16; i++) {
+    uint32_t a = w[i] & 0x7FFF7FFFu;
+    uint32_t lo = a & 0xFFFFu, hi = a >> 16;
+    m = max(m, max(lo, hi));
+  }
+  const uint32_t code = e8m0_from_amax_bits(m);
+  const float s = e8m0_to_f32(code);
+#pragma unroll
+  for (int d = 0; d < 4; d++) {
+    uint32_t o = 0;
+    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[4 * d + 0]), s, 0);
+    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[4 * d + 1]), s, 1);
+    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[4 * d + 2]), s, 2);
+    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[4 * d + 3]), s, 3);
+    out[d] = o;
+  }
+  return code;
+}
+
+// 16-byte streaming load (non-temporal hint: the data is read once).
+__device__ __forceinline__ uint4 load_nt16(const void* p) {
+  const v4i v = __builtin_nontemporal_load((const v4i*)p);
+  return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
+}
+
+__device__ __forceinline__ v4s lds_read_tr16(const FT_LDS void* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((FT_LDS v4s*)p);
+}
+
+__device__ __forceinline__ v2i lds_read_tr4(const FT_LDS void* p) {
+  return __builtin_amdgcn_ds_read_tr4_b64_v2i32((FT_LDS v2i*)p);
+}
+
+__device__ __forceinline__ v8bf make_v8bf(v4s a, v4s b) {
+  struct { v4s x, y; } t = {a, b};
+  return __builtin_bit_cast(v8bf, t);
+}
+
+__device__ __forceinline__ v8bf pack_v8bf(const uint32_t (&h)[8]) {
+  v4i t;
+  t[0] = (int)(h[0] | (h[1] << 16));
+  t[1] = (int)(h[2] | (h[3] << 16));
+  t[2] = (int)(h[4] | (h[5] << 16));
+  t[3] = (int)(h[6] | (h[7] << 16));
+  return __builtin_bit_cast(v8bf, t);
+}
+
+__device__ __forceinline__ v16f mfma_bf16_32x32x16(v8bf a, v8bf b, v16f c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// FP4 x FP4 block-scaled MFMA.  a, b: 16 packed bytes each (upper half of the
+// 8-dword operand unused for FP4).  sa, sb: E8M0 bytes, byte SEL of the word.
+template <int SEL>
+__device__ __forceinline__ v16f mfma_fp4_32x32x64(v4i a, v4i b, v16f c, int sa, int sb) {
+  v8i a8 = {a[0], a[1], a[2], a[3], 0, 0, 0, 0};
+  v8i b8 = {b[0], b[1], b[2], b[3], 0, 0, 0, 0};
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, SEL, sa, SEL, sb);
+}
+
+}  // namespace ft

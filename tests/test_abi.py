@@ -1,0 +1,114 @@
+"""The C ABI library loads, exports every entry point its header declares, and
+rejects invalid arguments before launching anything (CPU only: none of these
+calls reaches a kernel launch)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_05711_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fourtune.h")
+
+def _gpu_visible():
+    import torch
+    return torch.cuda.is_available()
+
+
+# The validation tests pass fake device addresses that a correct library never
+# dereferences; they run only where no GPU is visible, so that a regression in
+# validation can never turn into a launch on bogus pointers.
+pytestmark = [pytest.mark.skipif(not os.path.exists(_lib.LIB_PATH), reason="libfourtune.so not built"),
+              pytest.mark.skipif(_gpu_visible(), reason="host-logic checks with fake pointers run without a GPU")]
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ft_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("ft_quantize_blockwise", "ft_linear_fwd", "ft_linear_bwd_input", "ft_lora_grads",
+              "ft_status_string", "ft_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings():
+    L = _lib.load()
+    for code, text in [(0, "ok"), (1, "null pointer"), (2, "invalid shape"), (3, "misaligned pointer"),
+                       (4, "unsupported argument"), (5, "HIP runtime error")]:
+        assert _lib.status_string(code) == text
+    assert _lib.status_string(99) == "unknown status"
+    assert L.ft_last_error() is not None
+
+
+ALIGNED = ctypes.c_void_p(0x100000)      # never dereferenced: validation fails first
+ALIGNED2 = ctypes.c_void_p(0x200000)
+MISALIGNED = ctypes.c_void_p(0x100008)
+NULL = None
+
+
+def q(src, rows, cols, block_rows, codes, scales, proj=NULL, R=0, layout=0, out=NULL):
+    return _lib.load().ft_quantize_blockwise(src, rows, cols, block_rows, codes, scales, proj, R, layout, out, NULL)
+
+
+def test_quantize_validation():
+    assert q(ALIGNED, 4, 48, 1, ALIGNED, ALIGNED) == _lib.FT_ERR_SHAPE          # cols % 32
+    assert q(ALIGNED, -1, 64, 1, ALIGNED, ALIGNED) == _lib.FT_ERR_SHAPE
+    assert q(ALIGNED, 48, 64, 32, ALIGNED, ALIGNED) == _lib.FT_ERR_SHAPE        # rows % 32 for tiles
+    assert q(ALIGNED, 4, 64, 2, ALIGNED, ALIGNED) == _lib.FT_ERR_UNSUPPORTED
+    assert q(NULL, 4, 64, 1, ALIGNED, ALIGNED) == _lib.FT_ERR_NULL
+    assert q(MISALIGNED, 4, 64, 1, ALIGNED, ALIGNED) == _lib.FT_ERR_ALIGN
+    assert q(ALIGNED, 4, 64, 1, ALIGNED, ALIGNED, ALIGNED2, 20, 0, ALIGNED2) == _lib.FT_ERR_UNSUPPORTED
+    assert q(ALIGNED, 4, 64, 1, ALIGNED, ALIGNED, ALIGNED2, 144, 0, ALIGNED2) == _lib.FT_ERR_UNSUPPORTED
+    assert q(ALIGNED, 4, 64, 1, ALIGNED, ALIGNED, ALIGNED2, 32, 0, NULL) == _lib.FT_ERR_NULL
+    assert q(ALIGNED, 4, 64, 1, ALIGNED, ALIGNED, ALIGNED2, 32, 7, ALIGNED2) == _lib.FT_ERR_UNSUPPORTED
+    assert q(ALIGNED, 64, 64, 32, ALIGNED, ALIGNED, ALIGNED2, 32, 0, ALIGNED2) == _lib.FT_ERR_UNSUPPORTED
+    # empty input is a no-op, even with NULL buffers
+    assert q(NULL, 0, 64, 1, NULL, NULL) == _lib.FT_OK
+
+
+def test_linear_validation():
+    L = _lib.load()
+    f = L.ft_linear_fwd
+    assert f(ALIGNED, ALIGNED, 8, 48, ALIGNED, ALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_SHAPE
+    assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 40, NULL, 0, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_SHAPE
+    assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 3, NULL) == _lib.FT_ERR_UNSUPPORTED
+    assert f(ALIGNED, NULL, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_NULL
+    assert f(MISALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_ALIGN
+    assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, ALIGNED2, 32, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_NULL
+    assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, ALIGNED2, 24, ALIGNED2, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_UNSUPPORTED
+    assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, ALIGNED2, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_UNSUPPORTED
+    assert f(ALIGNED, ALIGNED, 8, 0, ALIGNED, ALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_SHAPE
+    assert f(NULL, NULL, 0, 64, NULL, NULL, 64, NULL, 0, NULL, NULL, NULL, 0, NULL) == _lib.FT_OK
+    b = L.ft_linear_bwd_input
+    assert b(ALIGNED, ALIGNED, 8, 48, ALIGNED, ALIGNED, 64, NULL, 0, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_SHAPE
+    assert b(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, ALIGNED2, 32, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_NULL
+    assert b(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, MISALIGNED, 1, NULL) == _lib.FT_ERR_ALIGN
+    assert b(NULL, NULL, 0, 64, NULL, NULL, 64, NULL, 0, NULL, NULL, 0, NULL) == _lib.FT_OK
+
+
+def test_lora_validation():
+    f = _lib.load().ft_lora_grads
+    args = lambda **kw: [kw.get("x", ALIGNED), kw.get("M", 8), kw.get("K", 64), kw.get("dy", ALIGNED), kw.get("N", 64),
+                         kw.get("xa", ALIGNED2), kw.get("dyb", ALIGNED2), kw.get("ld", 32), kw.get("r", 16),
+                         kw.get("dA", ALIGNED), kw.get("dB", ALIGNED), kw.get("acc", 0), NULL]
+    assert f(*args(r=0)) == _lib.FT_ERR_UNSUPPORTED
+    assert f(*args(r=129, ld=132)) == _lib.FT_ERR_UNSUPPORTED
+    assert f(*args(ld=8)) == _lib.FT_ERR_SHAPE
+    assert f(*args(ld=33)) == _lib.FT_ERR_SHAPE
+    assert f(*args(K=40)) == _lib.FT_ERR_SHAPE
+    assert f(*args(acc=2)) == _lib.FT_ERR_UNSUPPORTED
+    assert f(*args(dA=NULL)) == _lib.FT_ERR_NULL
+    assert f(*args(x=NULL)) == _lib.FT_ERR_NULL
+    assert f(*args(dy=MISALIGNED)) == _lib.FT_ERR_ALIGN
