@@ -125,4 +125,54 @@ __device__ __forceinline__ v16f mfma_fp4_32x32x64(v4i a, v4i b, v16f c, int sa, 
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, SEL, sa, SEL, sb);
 }
 
+// Raw buffer resource over [base, base + bytes): loads at offsets >= bytes
+// return zeros, which handles ragged tiles without branches.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// An offset no buffer here reaches: a load from it returns zeros.
+constexpr uint32_t kOobOffset = 0x80000000u;
+
+// 16 bytes per lane from a buffer into LDS at lds_base + 16 * lane
+// (lds_base must be the same for the whole wave).
+__device__ __forceinline__ void buffer_to_lds16(__amdgpu_buffer_rsrc_t r, FT_LDS void* lds_base, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_base, 16, voff, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint2 buffer_load8(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  const v2i v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, 0, 0);
+  return make_uint2((uint32_t)v[0], (uint32_t)v[1]);
+}
+
+__device__ __forceinline__ uint32_t buffer_load_u8(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(r, voff, 0, 0);
+}
+
+// Buffer resource words for the asm loads below (same layout as make_rsrc).
+__device__ __forceinline__ v4i rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  return v4i{(int)(uint32_t)a, (int)(uint32_t)(a >> 32) & 0xFFFF, (int)bytes, 0x00020000};
+}
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const FT_LDS void*)p;
+}
+
+// Buffer -> LDS loads issued as inline asm: lane L writes lds_base + 16L (or
+// + 4L).  The compiler does not see these as LDS writes, so it never adds
+// waits for them; callers publish the data with an explicit vmcnt wait and a
+// barrier.  lds_base must be wave-uniform.
+// The byte offset is voff (per lane) + soff (uniform); a voff at or beyond the
+// buffer size reads zeros whatever soff is.
+__device__ __forceinline__ void dma16(v4i rsrc, uint32_t lds_base, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds_base), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(v4i rsrc, uint32_t lds_base, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+               :: "s"(lds_base), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+}
+
 }  // namespace ft

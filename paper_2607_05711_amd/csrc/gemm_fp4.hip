@@ -14,6 +14,8 @@
 // lane).  Reduction staged 256 elements (128 bytes of codes per row) at a
 // time, double-buffered through LDS with a 16-byte row pad, loads for stage
 // s+1 in flight while stage s runs on the matrix cores.
+#include <type_traits>
+
 #include "ft_device.h"
 #include "ft_kernels.h"
 
@@ -26,7 +28,7 @@ constexpr int GSTRIDE = GROW + 16;      // padded LDS row stride (bytes)
 constexpr int GTILE = GB * GSTRIDE;     // bytes per operand tile per stage
 
 template <bool BWD, bool OUT_F32>
-__global__ __launch_bounds__(256, 1) void k_gemm_fp4(const uint8_t* __restrict__ A, const uint8_t* __restrict__ As,
+__global__ __launch_bounds__(256, 1) void k_gemm_fp4_generic(const uint8_t* __restrict__ A, const uint8_t* __restrict__ As,
                                                      const uint8_t* __restrict__ Wq, const uint8_t* __restrict__ Ws,
                                                      int M, int N, int K, const float* __restrict__ P, int R,
                                                      const uint16_t* __restrict__ LR,
@@ -224,17 +226,480 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4(const uint8_t* __restrict__
   }
 }
 
+
+// ============================================================== fast path
+// Pipelined kernel for reduction lengths that are multiples of 128 (and, for
+// the backward, K a multiple of 128).  Every stage of work moves through a
+// 4-slot LDS ring with buffer loads that write LDS directly; rows past the
+// matrix edge read as zeros through the buffer range check, so tiles need no
+// branches.  Three stages are in flight while one runs on the matrix cores.
+//
+// Stage kinds:
+//   FP4 stage: 128 reduction elements.  Slot = A tile [256 rows][64 B] +
+//     W tile (forward [256 n][64 B]; backward [128 n][128 B], read with the
+//     nibble-transposing LDS read) + the stage's E8M0 scales.
+//   Low-rank stage (after the FP4 stages): 16 columns of the up-projection.
+//     Slot = P chunk [256 rows][16 fp32] + U chunk (forward, [16 j][256 n]
+//     bf16) or D chunk (backward, [256 k][16 j] bf16).  P is split into two
+//     bf16 terms in registers; its product lands in the same accumulators.
+// Within a stage, the barrier that publishes the next stage sits between the
+// two k-steps, so the next stage's first fragments load under the current
+// MFMAs.  The finished tile is staged through LDS for coalesced stores.
+
+constexpr int PK = 128;                  // reduction elements per FP4 stage
+constexpr int PROW = PK / 2;             // bytes per A-tile row per stage
+constexpr int SLOT = 36 * 1024;          // bytes per ring slot
+constexpr int NSLOT = 4;
+constexpr int OFF_B = 16 * 1024;         // W tile / U / D chunk within a slot
+constexpr int OFF_SA = 32 * 1024;        // A scales: 256 rows x 4 bytes
+constexpr int OFF_SB = 33 * 1024;        // W scales: 4 waves x 256 bytes
+constexpr int LOADS_FP4 = 10;            // buffer loads per wave per FP4 stage
+constexpr int LOADS_LR = 6;              // ... per low-rank stage
+
+// 16-byte chunk swizzles: 64-byte rows (4 chunks) and 128-byte rows (8 chunks)
+__device__ __forceinline__ int swz64(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
+__device__ __forceinline__ int swz128(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// Workgroup id -> output tile.  Consecutive ids go to different XCDs, so each
+// XCD gets a contiguous range of tiles; within it tiles run in groups of 4
+// tile-rows, which keeps their A rows and W columns together in that XCD's L2.
+__device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, int& mt, int& nt) {
+  const int T = tiles_m * tiles_n;
+  int t = bid;
+  if (T % 8 == 0) t = (bid & 7) * (T >> 3) + (bid >> 3);
+  constexpr int GM = 4;
+  const int gsize = GM * tiles_n;
+  const int g = t / gsize, first = g * GM;
+  const int gm = min(GM, tiles_m - first);
+  const int w = t - g * gsize;
+  mt = first + w % gm;
+  nt = w / gm;
+}
+
+template <int N_>
+__device__ __forceinline__ void wait_vm() {
+  // vmcnt(N_) with expcnt/lgkmcnt left unconstrained (gfx9 encoding)
+  __builtin_amdgcn_s_waitcnt((N_ & 15) | ((N_ >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <bool BWD, bool OUT_F32>
+__global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restrict__ A, const uint8_t* __restrict__ As,
+                                                          const uint8_t* __restrict__ Wq, const uint8_t* __restrict__ Ws,
+                                                          int M, int N, int K, const float* __restrict__ P, int R,
+                                                          const uint16_t* __restrict__ LR,
+                                                          const uint16_t* __restrict__ bias, void* __restrict__ out,
+                                                          int tiles_m, int tiles_n) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[NSLOT * SLOT];
+
+  const int NO = BWD ? K : N;
+  const int KR = BWD ? N : K;
+  const int lda = KR >> 1, nkb = KR >> 5, ldw = K >> 1, nwkb = K >> 5;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: keeps LDS bases in SGPRs
+  const int r32 = lane & 31, h = lane >> 5, g16 = lane >> 4, t16 = lane & 15;
+  const int wm = wave >> 1, wn = wave & 1;
+  int mt, nt;
+  tile_coords(blockIdx.x, tiles_m, tiles_n, mt, nt);
+  const int m0 = mt * GB, n0 = nt * GB;
+
+  const v4i ra = rsrc_words(A, (uint32_t)M * lda);
+  const v4i rw = rsrc_words(Wq, (uint32_t)N * ldw);
+  const v4i ras = rsrc_words(As, (uint32_t)M * nkb);
+  const v4i rws = rsrc_words(Ws, (uint32_t)(N >> 5) * nwkb);
+  const v4i rp = rsrc_words(P, (uint32_t)M * R * 4);
+  const v4i rl = rsrc_words(LR, (uint32_t)(BWD ? K : N) * R * 2);
+  const uint32_t lds0 = lds_addr(lds);
+
+  const int nst = KR / PK, nlr = R / 16, total = nst + nlr;
+
+  // ---------------- per-lane load geometry (constant over stages)
+  // Each buffer load takes a per-lane byte offset (constant over stages; rows
+  // outside the matrix hold kOobOffset, which reads zeros) plus a uniform
+  // per-stage offset.
+  // 64-byte-row tiles (A, forward W, P chunk): instruction i of this wave
+  // fills rows wave*64 + 16i + [0,16); lane L -> row + L/4, chunk (L%4)^swz64.
+  const int r64 = wave * 64 + (lane >> 2);
+  const int c64 = (lane & 3) ^ swz64(lane >> 2);
+  uint32_t a_base[4], w_base[4], p_base[4];
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const int r = r64 + 16 * i;
+    a_base[i] = (m0 + r < M) ? (uint32_t)(m0 + r) * lda + c64 * 16 : kOobOffset;
+    p_base[i] = (m0 + r < M) ? (uint32_t)(m0 + r) * R * 4 + c64 * 16 : kOobOffset;
+    w_base[i] = kOobOffset;
+    if constexpr (!BWD) w_base[i] = (n0 + r < N) ? (uint32_t)(n0 + r) * ldw + c64 * 16 : kOobOffset;
+  }
+  // backward W tile: 128 reduction rows x 128 bytes; instruction i fills rows
+  // wave*32 + 8i + [0,8); lane L -> row + L/8, chunk (L%8) ^ swz128(row).
+  const int rb128 = wave * 32 + (lane >> 3);
+  const int cb128 = (lane & 7) ^ swz128(lane >> 3);
+  uint32_t wt_base[4];
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const int byte = (n0 >> 1) + ((cb128 ^ (i & 1)) * 16);
+    wt_base[i] = (byte < ldw) ? (uint32_t)(rb128 + 8 * i) * ldw + byte : kOobOffset;
+  }
+  // scales: wave w stages A-scale dwords of tile rows 64w + lane; W scales:
+  //   forward: lanes 0,1 of wave w fetch 32-column blocks 2w, 2w+1 of the tile;
+  //   backward: lanes 0,1 of wave w fetch W-scale row (stage*4 + w), blocks 4*lane..+3.
+  const uint32_t sa_base = (m0 + wave * 64 + lane < M) ? (uint32_t)(m0 + wave * 64 + lane) * nkb : kOobOffset;
+  uint32_t sb_base = kOobOffset;
+  if (lane < 2) {
+    if constexpr (!BWD) {
+      const int nb = (n0 >> 5) + 2 * wave + lane;
+      if (nb < (N >> 5)) sb_base = (uint32_t)nb * nwkb;
+    } else {
+      const int kb = (n0 >> 5) + 4 * lane;
+      if (kb < (K >> 5)) sb_base = (uint32_t)wave * nwkb + kb;
+    }
+  }
+  // low-rank chunk geometry
+  //   forward U chunk [16 j][256 n] (512-byte rows): instruction i fills rows
+  //     2i, 2i+1 (waves 0..3 own instructions 2w, 2w+1); lane L -> row + L/32,
+  //     chunk (L%32) ^ (2*(row&3)).
+  //   backward D chunk [256 k][16 j] (32-byte rows): instruction i fills rows
+  //     32i + [0,32) (waves own 2w, 2w+1); lane L -> row + L/2, half (L%2)^((row>>2)&1).
+  uint32_t l_base[2];
+#pragma unroll
+  for (int i = 0; i < 2; i++) {
+    const int ins = 2 * wave + i;
+    if constexpr (!BWD) {
+      const int j = 2 * ins + (lane >> 5);
+      const int c = (lane & 31) ^ (2 * (j & 3));
+      l_base[i] = (n0 + c * 8 < N) ? (uint32_t)j * N * 2 + (uint32_t)(n0 + c * 8) * 2 : kOobOffset;
+    } else {
+      const int k = 32 * ins + (lane >> 1);
+      const int c = (lane & 1) ^ ((k >> 2) & 1);
+      l_base[i] = (n0 + k < K) ? (uint32_t)(n0 + k) * R * 2 + c * 16 : kOobOffset;
+    }
+  }
+
+  auto slot_of = [&](int t) { return (uint32_t)((t & (NSLOT - 1)) * SLOT); };
+
+  // ---------------- stage loads (LDS destinations and per-stage offsets are uniform)
+  auto issue_fp4 = [&](int t) {
+    const uint32_t slot = lds0 + slot_of(t);
+    const uint32_t sa_off = (uint32_t)t * PROW;
+#pragma unroll
+    for (int i = 0; i < 4; i++) dma16(ra, slot + (wave * 64 + 16 * i) * PROW, a_base[i], sa_off);
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      if constexpr (!BWD) dma16(rw, slot + OFF_B + (wave * 64 + 16 * i) * PROW, w_base[i], sa_off);
+      else dma16(rw, slot + OFF_B + (wave * 32 + 8 * i) * 128, wt_base[i], (uint32_t)t * PK * ldw);
+    }
+    dma4(ras, slot + OFF_SA + wave * 256, sa_base, (uint32_t)t * 4);
+    if constexpr (!BWD) dma4(rws, slot + OFF_SB + wave * 256, sb_base, (uint32_t)t * 4);
+    else dma4(rws, slot + OFF_SB + wave * 256, sb_base, (uint32_t)t * 4 * nwkb);
+  };
+  auto issue_lr = [&](int t) {
+    const uint32_t slot = lds0 + slot_of(t);
+    const int q = t - nst;
+#pragma unroll
+    for (int i = 0; i < 4; i++) dma16(rp, slot + (wave * 64 + 16 * i) * 64, p_base[i], (uint32_t)q * 64);
+#pragma unroll
+    for (int i = 0; i < 2; i++)
+      dma16(rl, slot + OFF_B + (2 * wave + i) * 1024, l_base[i], BWD ? (uint32_t)q * 32 : (uint32_t)q * 16 * N * 2);
+  };
+  auto issue = [&](int t) {
+    if (t >= total) return;
+    if (t < nst) issue_fp4(t);
+    else issue_lr(t);
+  };
+
+  // Loads one wave issues for stage u (0 past the end).
+  auto loads_of = [&](int u) { return u >= total ? 0 : (u < nst ? LOADS_FP4 : LOADS_LR); };
+  // Wait until at most n of this wave's loads are outstanding, then barrier:
+  // with n = the loads issued after stage u, stage u is in LDS for every wave.
+  auto publish = [&](int n) {
+    switch (n) {
+      case 0: wait_vm<0>(); break;
+      case LOADS_LR: wait_vm<LOADS_LR>(); break;
+      case LOADS_FP4: wait_vm<LOADS_FP4>(); break;
+      case 2 * LOADS_LR: wait_vm<2 * LOADS_LR>(); break;
+      case LOADS_FP4 + LOADS_LR: wait_vm<LOADS_FP4 + LOADS_LR>(); break;
+      default: wait_vm<2 * LOADS_FP4>(); break;
+    }
+    // plain barrier: the LDS data it publishes was written by buffer loads,
+    // whose completion the vmcnt wait above already covers
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");     // no LDS read moves above the barrier
+  };
+
+  // ---------------- fragment reads
+  const int sw_a = swz64(r32);                      // rows ... + r32 of 64-byte-row tiles
+  const int sw_t = (t16 & 7) ^ ((t16 >> 3) & 1);    // rows ... + t16 of the backward W tile
+  const uint32_t psel = h ? 0x0301u : 0x0200u;      // result bytes 0,1 = scale bytes h, h+2 of a dword
+
+  // Per-lane LDS read offsets within a slot, one set per k-step (a fragment
+  // read is then one address add plus an immediate offset).
+  uint32_t rd_a[2], rd_b[2], rd_t[2][4];
+#pragma unroll
+  for (int kk = 0; kk < 2; kk++) {
+    rd_a[kk] = (wm * 128 + r32) * PROW + (((2 * kk + h) ^ sw_a) << 4);
+    rd_b[kk] = OFF_B + (wn * 128 + r32) * PROW + (((2 * kk + h) ^ sw_a) << 4);
+#pragma unroll
+    for (int j = 0; j < 4; j++)
+      rd_t[kk][j] = OFF_B + (kk * 64 + 32 * h + t16) * 128 + (((wn * 4 + j) ^ sw_t) << 4) + 8 * (g16 & 1);
+  }
+  const uint32_t rd_sa = OFF_SA + (wm * 128 + r32) * 4;
+  const uint32_t rd_sbt = OFF_SB + h * 256 + wn * 4;     // backward W-scale rows h (+2)
+
+  struct Fp4Frag { v4i a[4], b[4]; };
+  auto read_fp4 = [&](int t, int kk, Fp4Frag& f) {
+    const uint8_t* slot = lds + slot_of(t);
+    const uint8_t* pa = slot + rd_a[kk];
+#pragma unroll
+    for (int i = 0; i < 4; i++) f.a[i] = *(const v4i*)(pa + i * 32 * PROW);
+    if constexpr (!BWD) {
+      const uint8_t* pb = slot + rd_b[kk];
+#pragma unroll
+      for (int j = 0; j < 4; j++) f.b[j] = *(const v4i*)(pb + j * 32 * PROW);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const uint8_t* pt = slot + rd_t[kk][j];
+        const v2i lo = lds_read_tr4((const FT_LDS void*)pt);
+        const v2i hi = lds_read_tr4((const FT_LDS void*)(pt + 16 * 128));
+        f.b[j] = v4i{lo[0], lo[1], hi[0], hi[1]};
+      }
+    }
+  };
+  // Raw scale words of a stage; turned into MFMA scale operands (one byte per
+  // k-step) only when the stage's MFMAs are about to issue.
+  struct ScaleRaw { uint32_t a[4], b[4]; };
+  auto read_scales = [&](int t, ScaleRaw& r) {
+    const uint8_t* slot = lds + slot_of(t);
+#pragma unroll
+    for (int i = 0; i < 4; i++) r.a[i] = *(const uint32_t*)(slot + rd_sa + i * 128);
+    if constexpr (!BWD) {
+#pragma unroll
+      for (int j = 0; j < 4; j++) {  // 32-column block wn*4 + j, staged by wave (wn*4+j)/2
+        r.b[j] = *(const uint32_t*)(slot + OFF_SB + (wn * 2 + (j >> 1)) * 256 + (j & 1) * 4);
+      }
+    } else {
+      // rows 2kk + h of this stage's W-scale block (staged by wave 2kk+h), column blocks wn*4 + j
+      r.b[0] = *(const uint32_t*)(slot + rd_sbt);
+      r.b[1] = *(const uint32_t*)(slot + rd_sbt + 512);
+    }
+  };
+  auto scale_ops = [&](const ScaleRaw& r, uint32_t (&sa)[4], uint32_t (&sb)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; i++) sa[i] = __builtin_amdgcn_perm(0u, r.a[i], psel);
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      if constexpr (!BWD) sb[j] = __builtin_amdgcn_perm(0u, r.b[j], psel);
+      else sb[j] = __builtin_amdgcn_perm(r.b[1], r.b[0], 0x0c0c0400u | (j << 8) | j);
+    }
+  };
+
+  struct LrFrag { v4i p[4][2]; v8bf b[4]; };
+  const int jj = t16 >> 2, qq = t16 & 3;
+  auto read_lr = [&](int t, LrFrag& f) {
+    const uint8_t* slot = lds + slot_of(t);
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const uint8_t* row = slot + (wm * 128 + i * 32 + r32) * 64;
+      f.p[i][0] = *(const v4i*)(row + (((2 * h) ^ sw_a) << 4));
+      f.p[i][1] = *(const v4i*)(row + (((2 * h + 1) ^ sw_a) << 4));
+    }
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      if constexpr (!BWD) {
+        const int n = wn * 128 + j * 32 + 16 * (g16 & 1) + 4 * qq;
+        const int row0 = 8 * h + jj;
+        const int byte0 = ((((n >> 3) ^ (2 * (row0 & 3))) << 4)) + ((n >> 2) & 1) * 8;
+        const v4s lo = lds_read_tr16((const FT_LDS void*)(slot + OFF_B + row0 * 512 + byte0));
+        const int row1 = row0 + 4;
+        const int byte1 = ((((n >> 3) ^ (2 * (row1 & 3))) << 4)) + ((n >> 2) & 1) * 8;
+        const v4s hi = lds_read_tr16((const FT_LDS void*)(slot + OFF_B + row1 * 512 + byte1));
+        f.b[j] = make_v8bf(lo, hi);
+      } else {
+        const int k = wn * 128 + j * 32 + r32;
+        f.b[j] = __builtin_bit_cast(v8bf, *(const v4i*)(slot + OFF_B + k * 32 + ((h ^ ((k >> 2) & 1)) << 4)));
+      }
+    }
+  };
+
+  v16f acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; i++)
+#pragma unroll
+    for (int j = 0; j < 4; j++) acc[i][j] = v16f{};
+
+  auto mfma_fp4_step = [&](int kk, const Fp4Frag& f, const uint32_t (&sa)[4], const uint32_t (&sb)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        if (kk == 0) acc[i][j] = mfma_fp4_32x32x64<0>(f.a[i], f.b[j], acc[i][j], (int)sa[i], (int)sb[j]);
+        else acc[i][j] = mfma_fp4_32x32x64<1>(f.a[i], f.b[j], acc[i][j], (int)sa[i], (int)sb[j]);
+      }
+  };
+  auto mfma_lr_step = [&](const LrFrag& f) {
+    v8bf ahi[4], alo[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const v4i x0 = f.p[i][0], x1 = f.p[i][1];
+      const int xs[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+      uint32_t hh[8], ll[8];
+#pragma unroll
+      for (int e = 0; e < 8; e++) split_bf16(__int_as_float(xs[e]), hh[e], ll[e]);
+      ahi[i] = pack_v8bf(hh);
+      alo[i] = pack_v8bf(ll);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        acc[i][j] = mfma_bf16_32x32x16(ahi[i], f.b[j], acc[i][j]);
+        acc[i][j] = mfma_bf16_32x32x16(alo[i], f.b[j], acc[i][j]);
+      }
+  };
+
+  // ---------------- pipeline
+  // Stage t's slot is refilled (with stage t+4) in iteration t+1, after that
+  // iteration's barrier; every wave passed its own wait for the reads of slot t
+  // (the wait at the top of iteration t+1) before arriving there.
+  issue(0);
+  issue(1);
+  issue(2);
+  publish(loads_of(1) + loads_of(2));
+  Fp4Frag f0, f1;
+  ScaleRaw sr;
+  read_fp4(0, 0, f0);
+  read_scales(0, sr);
+
+  // One FP4 iteration.  STEADY: stages t+1..t+3 are FP4 stages, so the body is
+  // branch-free with constant wait counts (no register copies of fragments).
+  auto fp4_iter = [&](int t, auto steady) {
+    constexpr bool S = decltype(steady)::value;
+    uint32_t sa[4], sb[4];
+    scale_ops(sr, sa, sb);               // reads issued a k-step ago: f0 and this stage's scales
+    __builtin_amdgcn_sched_barrier(0);
+    read_fp4(t, 1, f1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_fp4_step(0, f0, sa, sb);
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (S) {
+      wait_vm<LOADS_FP4>();              // stage t+1 landed; stage t+2 may stay in flight
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      issue_fp4(t + 3);                  // into the slot of stage t-1
+      read_fp4(t + 1, 0, f0);
+      read_scales(t + 1, sr);
+    } else {
+      publish(loads_of(t + 2));
+      issue(t + 3);
+      if (t + 1 < nst) {
+        read_fp4(t + 1, 0, f0);
+        read_scales(t + 1, sr);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_fp4_step(1, f1, sa, sb);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  int t = 0;
+#pragma unroll 1
+  for (; t + 3 < nst; t++) fp4_iter(t, std::true_type{});
+#pragma unroll 1
+  for (; t < nst; t++) fp4_iter(t, std::false_type{});
+  if (nlr > 0) {
+    LrFrag g;
+    read_lr(nst, g);
+#pragma unroll 1
+    for (int t = nst; t < total; t++) {
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // this wave's reads of slot t-1 are done
+      publish(loads_of(t + 2));
+      issue(t + 3);
+      LrFrag gn;
+      if (t + 1 < total) read_lr(t + 1, gn);
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_lr_step(g);
+      __builtin_amdgcn_sched_barrier(0);
+      g = gn;
+    }
+  }
+
+  // ---------------- epilogue: bias, convert, store
+  float bb[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (!BWD) {
+    if (bias) {
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const int gc = n0 + wn * 128 + j * 32 + r32;
+        bb[j] = gc < NO ? bf16_to_f32(bias[gc]) : 0.f;
+      }
+    }
+  }
+  if constexpr (OUT_F32) {
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int gc = n0 + wn * 128 + j * 32 + r32;
+      if (gc >= NO) continue;
+#pragma unroll
+      for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int v = 0; v < 16; v++) {
+          const int gr = m0 + wm * 128 + i * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+          if (gr < M) ((float*)out)[(size_t)gr * NO + gc] = acc[i][j][v] + bb[j];
+        }
+    }
+  } else {
+    // each wave stages its 128x128 bf16 sub-tile (row stride 272 bytes) and
+    // writes it back as 16-byte row segments
+    __syncthreads();  // all waves are done with the ring
+    constexpr int OS = 128 * 2 + 16;
+    uint8_t* ow = lds + wave * (128 * OS);
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+      for (int j = 0; j < 4; j++)
+#pragma unroll
+        for (int v = 0; v < 16; v++) {
+          const int rr = i * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+          const int cc = j * 32 + r32;
+          *(uint16_t*)(ow + rr * OS + cc * 2) = (uint16_t)f32_to_bf16_rne(acc[i][j][v] + bb[j]);
+        }
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+#pragma unroll
+    for (int it = 0; it < 32; it++) {
+      const int rr = it * 4 + (lane >> 4), cc = (lane & 15) * 8;
+      const int gr = m0 + wm * 128 + rr, gc = n0 + wn * 128 + cc;
+      const uint4 v = *(const uint4*)(ow + rr * OS + cc * 2);
+      if (gr < M && gc < NO) *(uint4*)((uint16_t*)out + (size_t)gr * NO + gc) = v;
+    }
+  }
+}
+
 hipError_t launch_gemm_fp4(bool bwd, const uint8_t* a, const uint8_t* as, const uint8_t* wq, const uint8_t* ws,
                            int M, int N, int K, const float* P, int R, const uint16_t* lr,
                            const uint16_t* bias, void* out, bool out_f32, hipStream_t st) {
   const int NO = bwd ? K : N;
-  dim3 grid((NO + GB - 1) / GB, (M + GB - 1) / GB);
+  const int KR = bwd ? N : K;
+  const int tm = (M + GB - 1) / GB, tn = (NO + GB - 1) / GB;
+  // buffer ranges are 32-bit: the pipelined kernel takes operands below 2 GiB
+  const bool small = (size_t)M * KR / 2 < (1u << 31) && (size_t)N * K / 2 < (1u << 31) &&
+                     (size_t)M * (R > 0 ? R : 1) * 4 < (1u << 31);
+  if (KR % PK == 0 && K % 128 == 0 && small) {
+    const unsigned grid = (unsigned)(tm * tn);
+    if (!bwd) {
+      if (out_f32) k_gemm_fp4_pipe<false, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out, tm, tn);
+      else k_gemm_fp4_pipe<false, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out, tm, tn);
+    } else {
+      if (out_f32) k_gemm_fp4_pipe<true, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out, tm, tn);
+      else k_gemm_fp4_pipe<true, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out, tm, tn);
+    }
+    return hipGetLastError();
+  }
+  dim3 grid(tn, tm);
   if (!bwd) {
-    if (out_f32) k_gemm_fp4<false, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out);
-    else k_gemm_fp4<false, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out);
+    if (out_f32) k_gemm_fp4_generic<false, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out);
+    else k_gemm_fp4_generic<false, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out);
   } else {
-    if (out_f32) k_gemm_fp4<true, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out);
-    else k_gemm_fp4<true, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out);
+    if (out_f32) k_gemm_fp4_generic<true, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out);
+    else k_gemm_fp4_generic<true, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out);
   }
   return hipGetLastError();
 }

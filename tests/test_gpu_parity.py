@@ -137,7 +137,7 @@ def run_gpu_layer(d, shape, with_bias=True):
         dA, dB = _lib.ft_lora_grads(X, dY, P, Qp, shape.r, col0=shape.r_s)
         out.update(dA=dA, dB=dB)
     torch.cuda.synchronize()
-    return {k: host(v) for k, v in out.items()}
+    return {k: host(v) for k, v in out.items() if v is not None}
 
 
 def check_layer(d, shape, g, rows=None, with_bias=True):
@@ -200,7 +200,9 @@ def test_lora_grads_accumulate():
     dA2, dB2 = dA.clone(), dB.clone()
     _lib.ft_lora_grads(X, dY, P, Qp, 32, col0=16, dA=dA2, dB=dB2, accumulate=True)
     torch.cuda.synchronize()
-    assert torch.allclose(dA2, 2 * dA, rtol=1e-5, atol=0) and torch.allclose(dB2, 2 * dB, rtol=1e-5, atol=0)
+    # atomics combine partial sums in any order: compare in norm, not per element
+    assert torch.linalg.norm(dA2 - 2 * dA) <= 1e-5 * torch.linalg.norm(dA)
+    assert torch.linalg.norm(dB2 - 2 * dB) <= 1e-5 * torch.linalg.norm(dB)
 
 
 def test_gemm_random_codes():
