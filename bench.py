@@ -15,6 +15,7 @@ Inputs are drawn on the device with a seeded generator and are resident in HBM
 when the timed region starts.  Prints one JSON line.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -44,7 +45,56 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="token rows in the oracle sample (0: auto)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB three times (scales HBM counters), then exit")
     return ap.parse_args()
+
+
+# Sources whose compiled code the GEMM traffic record was measured on; the record
+# is reported only while they hash the same.
+GEMM_SOURCES = ("paper_2607_05711_amd/csrc/gemm_fp4.hip", "paper_2607_05711_amd/csrc/ft_device.h",
+                "paper_2607_05711_amd/csrc/ft_kernels.h")
+TRAFFIC_RECORD = "profiles/gemm_fp4_flux_qkv_traffic.md"
+
+
+def sources_sha256(paths=GEMM_SOURCES):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(direction):
+    """HBM bytes per launch of the forward or backward-input GEMM from the
+    committed counter record (FETCH_SIZE + WRITE_SIZE, each scaled by the
+    factor a plain copy of known size gives), or None when the record is
+    missing or was taken on other kernel sources."""
+    path = os.path.join(ROOT, TRAFFIC_RECORD)
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as f:
+        for line in f:
+            m = line.strip().strip("`").split(":", 1)
+            if len(m) == 2 and m[0].strip().startswith(("source_sha256", "traffic_bytes_")):
+                rec[m[0].strip()] = m[1].strip()
+    if rec.get("source_sha256") != sources_sha256():
+        return None
+    v = rec.get("traffic_bytes_" + direction)
+    return float(v) if v else None
+
+
+def copy_calibration(mib):
+    import torch
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}), flush=True)
 
 
 def main():
@@ -54,6 +104,10 @@ def main():
         print("bench.py measures one GPU only: the layer's data-parallel shards are independent and this "
               "build runs no collectives; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
 
     import torch
     from paper_2607_05711_amd import _lib, gen
@@ -147,9 +201,10 @@ def main():
                    "M": M, "K": K, "N": N, "lora_rank": r, "stabilizer_rank": rs,
                    "outputs": "Y, dX bf16; dA, dB fp32", "parallelism": "single GPU"},
         "pct_mxfp4_peak": round(100.0 * tflops / MXFP4_PEAK_TFLOPS, 2),
-        "roofline": {"bound": "mfma", "kernel": "ft::k_gemm_fp4 (%s)" % ("backward-input" if gemm == "gemm_bwd" else "forward"),
+        "roofline": {"bound": "mfma", "kernel": "ft::k_gemm_fp4_pipe<%s> (%s)" % (("true, false", "backward-input") if gemm == "gemm_bwd" else ("false, false", "forward")),
                      "achieved": round(achieved, 1), "peak": MXFP4_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / MXFP4_PEAK_TFLOPS, 4), "traffic": None,
+                     "frac": round(achieved / MXFP4_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic("bwd" if gemm == "gemm_bwd" else "fwd"),
                      "per_launch_flops": gemm_flops, "avg_launch_us": round(avg_us[gemm], 2)},
         "kernels_us": {n: round(v, 2) for n, v in avg_us.items()},
         "kernels_frac": {
