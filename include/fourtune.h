@@ -143,11 +143,13 @@ ft_status ft_linear_bwd_input(const uint8_t *gq, const uint8_t *gs, int64_t M, i
  *   xa       fp32, row stride ld: columns [0, r) hold X A (pass P + r_s).
  *   dyb      fp32, row stride ld: columns [0, r) hold G B^T (pass Qp + r_s).
  *   ld       row stride of xa and dyb in elements (R); ld >= r, ld % 4 == 0.
+ *            xa and dyb are 16-byte aligned like every tensor (r_s % 4 == 0
+ *            when they point into P and Qp).
  *   r        1 <= r <= 128.
  *   dA       fp32 [K, r];  dB: fp32 [r, N].
  *   accumulate  0: overwrite dA and dB;  1: add into them.
  * Sums over M are combined across workgroups with atomic adds (last-bit
- * run-to-run variation).  K, N multiples of 32; M >= 0.
+ * run-to-run variation).  K, N multiples of 32 and at most 2^24; M >= 0.
  */
 ft_status ft_lora_grads(const void *x, int64_t M, int64_t K, const void *dy, int64_t N,
                         const float *xa, const float *dyb, int64_t ld, int32_t r,

@@ -141,8 +141,10 @@ ft_status ft_lora_grads(const void* x, int64_t M, int64_t K, const void* dy, int
   if (accumulate != 0 && accumulate != 1) return fail(FT_ERR_UNSUPPORTED, "accumulate = %d", accumulate);
   if (!dA || !dB) return fail(FT_ERR_NULL, "dA and dB are required");
   if (M > 0 && (!x || !dy || !xa || !dyb)) return fail(FT_ERR_NULL, "x, dy, xa and dyb are required");
-  if ((x && !aligned16(x)) || (dy && !aligned16(dy)) || !aligned16(dA) || !aligned16(dB))
-    return fail(FT_ERR_ALIGN, "x, dy, dA, dB must be 16-byte aligned");
+  if (K > (1 << 24) || N > (1 << 24)) return fail(FT_ERR_UNSUPPORTED, "K and N above 2^24 are not supported here");
+  if ((x && !aligned16(x)) || (dy && !aligned16(dy)) || (xa && !aligned16(xa)) || (dyb && !aligned16(dyb)) ||
+      !aligned16(dA) || !aligned16(dB))
+    return fail(FT_ERR_ALIGN, "x, dy, xa, dyb, dA, dB must be 16-byte aligned");
   return hip_status(ft::launch_lora_grads((const uint16_t*)x, (int)M, (int)K, (const uint16_t*)dy, (int)N, xa, dyb,
                                           (int)ld, r, dA, dB, accumulate != 0, stream),
                     "lora grads");

@@ -160,6 +160,13 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const FT_LDS void*)p;
 }
 
+// Wait until at most N_ vector memory operations of this wave are outstanding.
+template <int N_>
+__device__ __forceinline__ void wait_vm() {
+  // vmcnt(N_) with expcnt/lgkmcnt left unconstrained (gfx9 encoding)
+  __builtin_amdgcn_s_waitcnt((N_ & 15) | ((N_ >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // Buffer -> LDS loads issued as inline asm: lane L writes lds_base + 16L (or
 // + 4L).  The compiler does not see these as LDS writes, so it never adds
 // waits for them; callers publish the data with an explicit vmcnt wait and a

@@ -6,9 +6,6 @@
 
 namespace ft {
 
-// Quantize-rows kernel geometry: 4 waves x 32 rows, column chunks of QR_CW.
-constexpr int QR_ROWS = 128;
-constexpr int QR_CW = 384;
 
 hipError_t launch_quant_rows(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
                              const uint16_t* proj, int R, int layout, float* proj_out, hipStream_t st);

@@ -276,12 +276,6 @@ __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, i
   nt = w / gm;
 }
 
-template <int N_>
-__device__ __forceinline__ void wait_vm() {
-  // vmcnt(N_) with expcnt/lgkmcnt left unconstrained (gfx9 encoding)
-  __builtin_amdgcn_s_waitcnt((N_ & 15) | ((N_ >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 template <bool BWD, bool OUT_F32>
 __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restrict__ A, const uint8_t* __restrict__ As,
                                                           const uint8_t* __restrict__ Wq, const uint8_t* __restrict__ Ws,

@@ -1,128 +1,193 @@
-// Adapter weight gradients (FourTune Sec. 3.2):
+// Adapter weight gradients (FourTune Sec. 3.2, the gradients after Eq. 3):
 //   dB = (X A)^T G      dB[j,n] = sum_m xa[m,j]  G[m,n]
 //   dA = X^T (G B^T)    dA[k,j] = sum_m X[m,k]   gbt[m,j]
-// Both are out[j, c] = sum_m L[m, j] V[m, c] with a skinny fp32 L (r columns)
-// and a wide bf16 V, reduced over the token axis M.  The reduction axis is the
-// row axis of both operands in memory, so tiles are staged in LDS as stored
-// and the MFMA operands are gathered with transposing 16-bit LDS reads.  L is
-// split into two bf16 terms (hi + lo) so its ~16 leading bits take part.
-// Workgroups split M into chunks; their partial sums meet in fp32 atomics.
+// Both are sums over the token axis m of a skinny fp32 factor L[m, j]
+// (r columns) times a wide bf16 tensor V[m, c].  The reduction axis is the
+// row axis of both operands in memory, so 64-row stages of both are copied to
+// LDS as stored and the MFMA operands are gathered from there: V with the
+// transposing 16-bit LDS read, L with 32-bit reads, split into two bf16 terms
+// (hi + lo) so that its ~16 leading bits take part.
+//
+// Workgroup = 4 waves over 128 output columns (32 per wave) and one chunk of
+// the token axis; chunks meet in fp32 atomics.  Stages move through an LDS
+// ring with buffer loads that write LDS directly, one or two stages ahead of
+// the one on the matrix cores.  The two k-halves of an MFMA take the even and
+// odd rows of a 16-row step, which keeps the 32-bit L reads conflict-free.
+// dB's tile has j on the MFMA rows (A = L) and dA's has j on the columns
+// (B = L), so both store contiguous runs in their output layout.
 #include "ft_device.h"
 #include "ft_kernels.h"
 
 namespace ft {
 
-constexpr int LG_BC = 256;    // output columns per workgroup (4 waves x 2 tiles of 32)
-constexpr int LG_BM = 64;     // token rows per LDS stage
-constexpr int LG_VSTRIDE = LG_BC + 16;  // halfwords
+constexpr int LG_WC = 128;                    // output columns per workgroup
+constexpr int LG_BM = 64;                     // token rows per stage
+constexpr int LG_VROW = LG_WC * 2;            // bytes per V row in LDS
+constexpr int LG_VBYTES = LG_BM * LG_VROW;    // 16 KB
 
 template <int RTJ>
-struct LoraLds {
-  static constexpr int LSTRIDE = RTJ * 32 + 16;  // halfwords
-  static constexpr int V_HW = LG_BM * LG_VSTRIDE;
-  static constexpr int L_HW = LG_BM * LSTRIDE;
+struct LoraGeom {
+  static constexpr int LROW = RTJ * 128;                  // bytes per L row (RTJ*32 fp32)
+  static constexpr int LBYTES = LG_BM * LROW;
+  static constexpr int SLOT = LG_VBYTES + LBYTES;
+  static constexpr int NS = RTJ == 1 ? 3 : 2;             // ring slots
+  static constexpr int PD = NS - 1;                       // stages in flight ahead
+  static constexpr int V_LOADS = LG_VBYTES / 1024 / 4;    // per wave per stage
+  static constexpr int L_LOADS = LBYTES / 1024 / 4;
+  static constexpr int LOADS = V_LOADS + L_LOADS;
 };
 
 struct LoraJob {
-  const float* L;       // [M, ld], r columns used
-  const uint16_t* V;    // [M, C]
+  const float* L;       // [rows, ld] fp32; columns [0, r) used
+  const uint16_t* V;    // [rows, C] bf16
   float* out;
   int C;
   int out_rows_are_j;   // 1: out[j * C + c] (dB);  0: out[c * r + j] (dA)
-  int ncg;              // column groups
+  int ncg;              // column groups of LG_WC
+  uint32_t v_bytes;     // rows * C * 2  (< 2^31)
+  uint32_t l_bytes;     // rows * ld * 4 (< 2^31)
 };
+
+// 16-byte chunk swizzle of a V row (16 chunks): rows 0..7 of a group spread
+// their chunks over all 16 positions.
+__device__ __forceinline__ int lg_swz(int row, int chunk) { return chunk ^ ((row & 7) << 1); }
+
+// One workgroup's share: output columns [c0, c0 + LG_WC) of `job` over token
+// rows [mbeg, mend).  DB selects the operand roles and the store layout.
+template <int RTJ, bool DB>
+__device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int c0, int mbeg, int mend, int ld, int r) {
+  using G = LoraGeom<RTJ>;
+  const int nst = (mend - mbeg + LG_BM - 1) / LG_BM;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const v4i rv = rsrc_words(job.V, job.v_bytes);
+  const v4i rl = rsrc_words(job.L, job.l_bytes);
+  const uint32_t lds0 = lds_addr(lds);
+
+  // Per-lane DMA sources.  V load i of this wave fills LDS bytes
+  // [1024 (4 wave + i), +1024) of the stage's V area: rows 4(4 wave + i) + lane/16,
+  // physical chunk lane%16 holding logical chunk lg_swz(row, lane%16).
+  int v_row[G::V_LOADS];
+  uint32_t v_src[G::V_LOADS];
+#pragma unroll
+  for (int i = 0; i < G::V_LOADS; i++) {
+    const int row = 4 * (G::V_LOADS * wave + i) + (lane >> 4);
+    const int c = c0 + 8 * lg_swz(row, lane & 15);
+    v_row[i] = row;
+    v_src[i] = c < job.C ? (uint32_t)(row * job.C + c) * 2u : kOobOffset;
+  }
+  int l_row[G::L_LOADS];
+  uint32_t l_src[G::L_LOADS];
+#pragma unroll
+  for (int i = 0; i < G::L_LOADS; i++) {
+    const int byte = 1024 * (G::L_LOADS * wave + i) + 16 * lane;
+    const int row = byte / G::LROW, q = (byte % G::LROW) / 16;
+    l_row[i] = row;
+    l_src[i] = 4 * q < r ? (uint32_t)(row * ld + 4 * q) * 4u : kOobOffset;
+  }
+
+  auto issue = [&](int s) {
+    const int m0 = mbeg + s * LG_BM;
+    const uint32_t slot = lds0 + (uint32_t)((s % G::NS) * G::SLOT);
+    const uint32_t vs = (uint32_t)m0 * (uint32_t)job.C * 2u, ls = (uint32_t)m0 * (uint32_t)ld * 4u;
+#pragma unroll
+    for (int i = 0; i < G::V_LOADS; i++)
+      dma16(rv, slot + 1024 * (G::V_LOADS * wave + i), m0 + v_row[i] < mend ? v_src[i] : kOobOffset, vs);
+#pragma unroll
+    for (int i = 0; i < G::L_LOADS; i++)
+      dma16(rl, slot + LG_VBYTES + 1024 * (G::L_LOADS * wave + i), m0 + l_row[i] < mend ? l_src[i] : kOobOffset, ls);
+  };
+
+  // LDS read offsets within a slot.  V: source lane (jj, qq) of 16-lane group
+  // g16 reads row 2 jj + h (+8 for the second read, +16 per k-step) at
+  // logical column 32 wave + 16 (g16 & 1) + 4 qq.  L: lane (j, h) reads rows
+  // 2e + h (+16 per k-step) of column j.
+  const int g16 = lane >> 4, i16 = lane & 15, jj = i16 >> 2, qq = i16 & 3, h = g16 >> 1;
+  const int vr0 = 2 * jj + h;
+  const int vcol = 32 * wave + 16 * (g16 & 1) + 4 * qq;
+  const uint32_t v_rd = (uint32_t)(vr0 * LG_VROW + lg_swz(vr0, vcol >> 3) * 16 + (vcol & 7) * 2);
+  const uint32_t l_rd = (uint32_t)(LG_VBYTES + h * G::LROW + 4 * (lane & 31));
+
+  v16f acc[RTJ];
+#pragma unroll
+  for (int t = 0; t < RTJ; t++) acc[t] = v16f{};
+
+  issue(0);
+  if (G::PD > 1 && nst > 1) issue(1);
+#pragma unroll 1
+  for (int s = 0; s < nst; s++) {
+    if (G::PD > 1 && s + 1 < nst) wait_vm<G::LOADS>();
+    else wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");  // no LDS read moves above the barrier
+    if (s + G::PD < nst) issue(s + G::PD);
+
+    const FT_LDS uint8_t* sb = (const FT_LDS uint8_t*)lds + (s % G::NS) * G::SLOT;
+#pragma unroll
+    for (int ks = 0; ks < 4; ks++) {
+      const FT_LDS uint8_t* vp = sb + v_rd + ks * 16 * LG_VROW;
+      const v8bf vf = make_v8bf(lds_read_tr16(vp), lds_read_tr16(vp + 8 * LG_VROW));
+#pragma unroll
+      for (int t = 0; t < RTJ; t++) {
+        const FT_LDS float* lp = (const FT_LDS float*)(sb + l_rd + ks * 16 * G::LROW + t * 128);
+        uint32_t hi[8], lo[8];
+#pragma unroll
+        for (int e = 0; e < 8; e++) split_bf16(lp[2 * e * (G::LROW / 4)], hi[e], lo[e]);
+        const v8bf ah = pack_v8bf(hi), al = pack_v8bf(lo);
+        if constexpr (DB) {
+          acc[t] = mfma_bf16_32x32x16(ah, vf, acc[t]);
+          acc[t] = mfma_bf16_32x32x16(al, vf, acc[t]);
+        } else {
+          acc[t] = mfma_bf16_32x32x16(vf, ah, acc[t]);
+          acc[t] = mfma_bf16_32x32x16(vf, al, acc[t]);
+        }
+      }
+    }
+  }
+
+  // acc[t]: lane l, element v -> tile row 8(v/4) + 4h + v%4, tile column l%32.
+  // dB: rows are j (t*32 + row), columns c;  dA: rows are c, columns j.
+  const int l32 = lane & 31;
+#pragma unroll
+  for (int t = 0; t < RTJ; t++)
+#pragma unroll
+    for (int v = 0; v < 16; v++) {
+      const int tr = 8 * (v >> 2) + 4 * h + (v & 3);
+      const int j = DB ? t * 32 + tr : t * 32 + l32;
+      const int c = c0 + 32 * wave + (DB ? l32 : tr);
+      if (j < r && c < job.C) {
+        float* dst = DB ? job.out + (size_t)j * job.C + c : job.out + (size_t)c * r + j;
+        atomicAdd(dst, acc[t][v]);
+      }
+    }
+}
 
 template <int RTJ>
 __global__ __launch_bounds__(256) void k_lora_grads(LoraJob jb0, LoraJob jb1, int M, int ld, int r, int mchunk,
                                                     int nmch) {
-  using Lds = LoraLds<RTJ>;
-  __shared__ __attribute__((aligned(16))) uint16_t lv[Lds::V_HW];
-  __shared__ __attribute__((aligned(16))) uint16_t lhi[Lds::L_HW];
-  __shared__ __attribute__((aligned(16))) uint16_t llo[Lds::L_HW];
-
+  __shared__ __attribute__((aligned(16))) uint8_t lds[LoraGeom<RTJ>::NS * LoraGeom<RTJ>::SLOT];
   int b = blockIdx.x;
-  const int n0blocks = jb0.ncg * nmch;
-  const LoraJob job = b < n0blocks ? jb0 : jb1;
-  if (b >= n0blocks) b -= n0blocks;
+  const int n0 = jb0.ncg * nmch;
+  const bool second = b >= n0;
+  if (second) b -= n0;
+  const LoraJob& job = second ? jb1 : jb0;
   const int cg = b % job.ncg, mc = b / job.ncg;
-  const int c0 = cg * LG_BC;
   const int mbeg = mc * mchunk, mend = min(M, mbeg + mchunk);
+  if (job.out_rows_are_j) lora_tile<RTJ, true>(job, lds, cg * LG_WC, mbeg, mend, ld, r);
+  else lora_tile<RTJ, false>(job, lds, cg * LG_WC, mbeg, mend, ld, r);
+}
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int r32 = lane & 31, h = lane >> 5, g16 = lane >> 4, t16 = lane & 15;
-  const int jj = t16 >> 2, qq = t16 & 3;
-
-  v16f acc[RTJ][2];
-#pragma unroll
-  for (int t = 0; t < RTJ; t++) { acc[t][0] = v16f{}; acc[t][1] = v16f{}; }
-
-#pragma unroll 1
-  for (int m0 = mbeg; m0 < mend; m0 += LG_BM) {
-    // stage V[m0 .. m0+64) x [c0 .. c0+256)
-#pragma unroll
-    for (int i = 0; i < 8; i++) {
-      const int s = tid + 256 * i, row = s >> 5, col = (s & 31) * 8;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (m0 + row < mend && c0 + col < job.C)
-        v = load_nt16(job.V + (size_t)(m0 + row) * job.C + c0 + col);
-      *(uint4*)(lv + row * LG_VSTRIDE + col) = v;
-    }
-    // stage L[m0 .. m0+64) x [0 .. RTJ*32) as hi/lo bf16
-    constexpr int LEL = LG_BM * RTJ * 32;
-#pragma unroll
-    for (int i = 0; i < LEL / 256; i++) {
-      const int s = tid + 256 * i, row = s / (RTJ * 32), j = s % (RTJ * 32);
-      float x = 0.0f;
-      if (m0 + row < mend && j < r) x = job.L[(size_t)(m0 + row) * ld + j];
-      uint32_t hi, lo;
-      split_bf16(x, hi, lo);
-      lhi[row * Lds::LSTRIDE + j] = (uint16_t)hi;
-      llo[row * Lds::LSTRIDE + j] = (uint16_t)lo;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int ms = 0; ms < LG_BM / 16; ms++) {
-      const int mrow = ms * 16 + 8 * h + jj;   // this lane's source row for the first tr read
-      v8bf bv[2];
-#pragma unroll
-      for (int ct = 0; ct < 2; ct++) {
-        const int col = wave * 64 + ct * 32 + 16 * (g16 & 1) + 4 * qq;
-        const FT_LDS uint16_t* p = (FT_LDS uint16_t*)lv + mrow * LG_VSTRIDE + col;
-        bv[ct] = make_v8bf(lds_read_tr16(p), lds_read_tr16(p + 4 * LG_VSTRIDE));
-      }
-#pragma unroll
-      for (int t = 0; t < RTJ; t++) {
-        const int col = t * 32 + 16 * (g16 & 1) + 4 * qq;
-        const FT_LDS uint16_t* ph = (FT_LDS uint16_t*)lhi + mrow * Lds::LSTRIDE + col;
-        const FT_LDS uint16_t* pl = (FT_LDS uint16_t*)llo + mrow * Lds::LSTRIDE + col;
-        const v8bf ah = make_v8bf(lds_read_tr16(ph), lds_read_tr16(ph + 4 * Lds::LSTRIDE));
-        const v8bf al = make_v8bf(lds_read_tr16(pl), lds_read_tr16(pl + 4 * Lds::LSTRIDE));
-#pragma unroll
-        for (int ct = 0; ct < 2; ct++) {
-          acc[t][ct] = mfma_bf16_32x32x16(ah, bv[ct], acc[t][ct]);
-          acc[t][ct] = mfma_bf16_32x32x16(al, bv[ct], acc[t][ct]);
-        }
-      }
-    }
-    __syncthreads();
-  }
-
-  // acc[t][ct]: row j = t*32 + 8(v/4) + 4h + v%4, column c = c0 + wave*64 + ct*32 + r32
-#pragma unroll
-  for (int ct = 0; ct < 2; ct++) {
-    const int c = c0 + wave * 64 + ct * 32 + r32;
-    if (c >= job.C) continue;
-#pragma unroll
-    for (int t = 0; t < RTJ; t++)
-#pragma unroll
-      for (int v = 0; v < 16; v++) {
-        const int j = t * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-        if (j < r) {
-          float* dst = job.out_rows_are_j ? job.out + (size_t)j * job.C + c : job.out + (size_t)c * r + j;
-          atomicAdd(dst, acc[t][ct][v]);
-        }
-      }
-  }
+template <int RTJ>
+static void launch_lg(const LoraJob& jobB, const LoraJob& jobA, int rows, int ld, int r, hipStream_t st) {
+  // one round of workgroups: ring LDS allows two per CU up to RTJ 3, one at RTJ 4
+  const int slots = (2 * LoraGeom<RTJ>::NS * LoraGeom<RTJ>::SLOT <= 160 * 1024 ? 2 : 1) * 256;
+  const int ncg = jobB.ncg + jobA.ncg;
+  const int mblocks = (rows + LG_BM - 1) / LG_BM;
+  int nmch = std::max(1, std::min(mblocks, slots / ncg));
+  const int mchunk = ((mblocks + nmch - 1) / nmch) * LG_BM;
+  nmch = (rows + mchunk - 1) / mchunk;
+  k_lora_grads<RTJ><<<(unsigned)(ncg * nmch), 256, 0, st>>>(jobB, jobA, rows, ld, r, mchunk, nmch);
 }
 
 hipError_t launch_lora_grads(const uint16_t* x, int M, int K, const uint16_t* dy, int N, const float* xa,
@@ -135,21 +200,28 @@ hipError_t launch_lora_grads(const uint16_t* x, int M, int K, const uint16_t* dy
     if (e != hipSuccess) return e;
   }
   if (M == 0) return hipSuccess;
-  LoraJob jobB{xa, dy, dB, N, 1, (N + LG_BC - 1) / LG_BC};
-  LoraJob jobA{dyb, x, dA, K, 0, (K + LG_BC - 1) / LG_BC};
-  const int ncg = jobB.ncg + jobA.ncg;
-  const int mblocks = (M + LG_BM - 1) / LG_BM;
-  int nmch = std::max(1, std::min(mblocks, (1024 + ncg - 1) / ncg));
-  const int mchunk = ((mblocks + nmch - 1) / nmch) * LG_BM;
-  nmch = (M + mchunk - 1) / mchunk;
-  const unsigned grid = (unsigned)(ncg * nmch);
-  switch ((r + 31) / 32) {
-    case 1: k_lora_grads<1><<<grid, 256, 0, st>>>(jobB, jobA, M, ld, r, mchunk, nmch); break;
-    case 2: k_lora_grads<2><<<grid, 256, 0, st>>>(jobB, jobA, M, ld, r, mchunk, nmch); break;
-    case 3: k_lora_grads<3><<<grid, 256, 0, st>>>(jobB, jobA, M, ld, r, mchunk, nmch); break;
-    default: k_lora_grads<4><<<grid, 256, 0, st>>>(jobB, jobA, M, ld, r, mchunk, nmch); break;
+  // Token windows small enough that every buffer stays below 2 GiB, so the
+  // out-of-range offset used for masked lanes is beyond every buffer.
+  const size_t lim = (size_t)1 << 31;
+  size_t seg = std::min(lim / ((size_t)std::max(K, N) * 2), lim / ((size_t)ld * 4));
+  seg = std::min((size_t)M, seg / LG_BM * LG_BM);
+  if (seg == 0) return hipErrorInvalidValue;
+  for (size_t m0 = 0; m0 < (size_t)M; m0 += seg) {
+    const int rows = (int)std::min(seg, (size_t)M - m0);
+    const LoraJob jobB{xa + m0 * ld, dy + m0 * N, dB, N, 1, (N + LG_WC - 1) / LG_WC,
+                       (uint32_t)((size_t)rows * N * 2), (uint32_t)((size_t)rows * ld * 4)};
+    const LoraJob jobA{dyb + m0 * ld, x + m0 * K, dA, K, 0, (K + LG_WC - 1) / LG_WC,
+                       (uint32_t)((size_t)rows * K * 2), (uint32_t)((size_t)rows * ld * 4)};
+    switch ((r + 31) / 32) {
+      case 1: launch_lg<1>(jobB, jobA, rows, ld, r, st); break;
+      case 2: launch_lg<2>(jobB, jobA, rows, ld, r, st); break;
+      case 3: launch_lg<3>(jobB, jobA, rows, ld, r, st); break;
+      default: launch_lg<4>(jobB, jobA, rows, ld, r, st); break;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 }  // namespace ft

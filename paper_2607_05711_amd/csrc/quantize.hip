@@ -11,57 +11,96 @@
 namespace ft {
 
 // ---------------------------------------------------------------- rows
-// Workgroup = 4 waves; wave w owns 32 rows [row0 + 32w, +32) of one column
-// chunk of QR_CW columns.  Lane l holds row l%32 and, for block pair i, the
-// 32-element block 2i + l/32 of the chunk: it reads the block's 64 bytes,
-// quantizes it alone (no cross-lane reduction), and feeds the same registers
-// to the projection MFMAs.  The projection's reduction order is permuted to
-// match: MFMA q of pair i takes elements [8q, 8q+8) of each lane's block, and
-// the B operand is read from the same chunk positions.
+// Workgroup = WAVES waves over 32*WAVES rows x CW columns; wave w owns rows
+// [row0 + 32w, +32).  The wave walks its columns in steps of 64.  Loads are
+// row-contiguous: load q of a step brings rows 8q..8q+7, lane l taking
+// elements [8(l%8), +8) of row 8q + l/8, so every 8 lanes read one whole
+// 128-byte line.  A 32-element block then sits in 4 neighbouring lanes, which
+// reduce its absmax with two quad-permute DPP moves and each convert their 8
+// elements.  For the projection the wave writes the step's bf16 values to a
+// private LDS tile and reads them back in the MFMA operand layout (lane =
+// row), so the 32x32x16 bf16 MFMAs see the natural reduction order.
 //
-// proj chunk staged in LDS (zero padded to RT*32 columns and to QR_CW rows):
+// proj chunk staged in LDS (zero padded to RT*32 columns and to CW rows):
 //   MODE 1 (proj [cols, R]):  lds[k][j], row stride RT*32 + 16 halfwords;
 //     B fragments come from transposing reads (ds_read_b64_tr_b16).
-//   MODE 2 (proj [R, cols]):  lds[j][k], row stride QR_CW + 8 halfwords;
+//   MODE 2 (proj [R, cols]):  lds[j][k], row stride CW + 8 halfwords;
 //     B fragments are plain 16-byte reads.
-template <int RT, int MODE>
+constexpr int QR_XSTRIDE = 64 + 8;  // halfwords per row of a wave's 32x64 tile
+
+template <int RT, int MODE, int WAVES, int CW>
 struct QuantLds {
-  static constexpr int STRIDE = MODE == 1 ? RT * 32 + 16 : QR_CW + 8;   // halfwords
-  static constexpr int ROWS = MODE == 1 ? QR_CW : RT * 32;
-  static constexpr int HALFWORDS = MODE == 0 ? 8 : ROWS * STRIDE;
+  static constexpr int STRIDE = MODE == 1 ? RT * 32 + 16 : CW + 8;      // halfwords
+  static constexpr int ROWS = MODE == 1 ? CW : RT * 32;
+  static constexpr int PROJ_HW = MODE == 0 ? 0 : ROWS * STRIDE;
+  static constexpr int X_HW = MODE == 0 ? 0 : 32 * QR_XSTRIDE;          // per wave
+  static constexpr int HALFWORDS = MODE == 0 ? 8 : PROJ_HW + WAVES * X_HW;
 };
 
-template <int RT, int MODE>
-__global__ __launch_bounds__(256) void k_quant_rows(const uint16_t* __restrict__ src, int rows, int cols,
-                                                    uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
-                                                    const uint16_t* __restrict__ proj, int R,
-                                                    float* __restrict__ proj_out, int use_atomics) {
-  using L = QuantLds<RT, MODE>;
+// max over the 4 lanes of each aligned quad
+__device__ __forceinline__ uint32_t quad_max(uint32_t m) {
+  m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0xB1, 0xF, 0xF, true));  // quad_perm [1,0,3,2]
+  m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0x4E, 0xF, 0xF, true));  // quad_perm [2,3,0,1]
+  return m;
+}
+
+template <int RT, int MODE, int WAVES, int CW>
+__global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __restrict__ src, int rows,
+                                                                     int cols, uint8_t* __restrict__ codes,
+                                                                     uint8_t* __restrict__ scales,
+                                                                     const uint16_t* __restrict__ proj, int R,
+                                                                     float* __restrict__ proj_out, int use_atomics) {
+  using L = QuantLds<RT, MODE, WAVES, CW>;
   __shared__ __attribute__((aligned(16))) uint16_t lds[L::HALFWORDS];
+  constexpr int NST = CW / 64;     // 64-column steps per chunk
+  constexpr int NT = 64 * WAVES;   // threads
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int r32 = lane & 31, h = lane >> 5;
-  const int row = blockIdx.x * QR_ROWS + wave * 32 + r32;
-  const int c0 = blockIdx.y * QR_CW;
-  const int ncols = min(QR_CW, cols - c0);
+  const int rw0 = blockIdx.x * 32 * WAVES + wave * 32;  // first row of this wave
+  const int c0 = blockIdx.y * CW;
+  const int ncols = min(CW, cols - c0);
   const int nblk = ncols >> 5;
-  const bool row_ok = row < rows;
   const int nbc = cols >> 5;
+  const int lr = lane >> 3, lc = (lane & 7) * 8;     // row within an 8-row group, column within a step
+
+  // The first PF steps' loads go out before anything else; each step, once
+  // consumed, issues the load PF steps ahead.  Rows past the end and blocks
+  // past the chunk read an in-range address; their values become zeros.
+  constexpr int PF = NST < 6 ? NST : 6;
+  v4i xv[NST][4];
+  auto issue = [&](int st) {
+    const int col = min(64 * st + lc, ncols - 8);
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+      const int row = min(rw0 + 8 * q + lr, rows - 1);
+      xv[st][q] = *(const v4i*)(src + (size_t)row * cols + c0 + col);
+    }
+  };
+#pragma unroll
+  for (int st = 0; st < PF; st++) issue(st);
 
   if constexpr (MODE != 0) {
     // Stage the projection chunk: 16-byte slots, zero outside [R] x [ncols].
-    constexpr int SLOTS_PER_ROW = MODE == 1 ? RT * 4 : QR_CW / 8;
+    constexpr int SLOTS_PER_ROW = MODE == 1 ? RT * 4 : CW / 8;
     constexpr int NSLOTS = L::ROWS * SLOTS_PER_ROW;
-    for (int s = tid; s < NSLOTS; s += 256) {
+    constexpr int PER_THREAD = (NSLOTS + NT - 1) / NT;
+    uint4 v[PER_THREAD];
+#pragma unroll
+    for (int u = 0; u < PER_THREAD; u++) {
+      const int s = tid + NT * u;
       const int rr = s / SLOTS_PER_ROW, cc = (s % SLOTS_PER_ROW) * 8;
-      uint4 v = make_uint4(0, 0, 0, 0);
+      v[u] = make_uint4(0, 0, 0, 0);
       if constexpr (MODE == 1) {  // rr = k within chunk, cc = j
-        if (rr < ncols && cc < R) v = *(const uint4*)(proj + (size_t)(c0 + rr) * R + cc);
+        if (s < NSLOTS && rr < ncols && cc < R) v[u] = *(const uint4*)(proj + (size_t)(c0 + rr) * R + cc);
       } else {                    // rr = j, cc = k within chunk
-        if (rr < R && cc < ncols) v = *(const uint4*)(proj + (size_t)rr * cols + c0 + cc);
+        if (s < NSLOTS && rr < R && cc < ncols) v[u] = *(const uint4*)(proj + (size_t)rr * cols + c0 + cc);
       }
-      *(uint4*)(lds + rr * L::STRIDE + cc) = v;
+    }
+#pragma unroll
+    for (int u = 0; u < PER_THREAD; u++) {
+      const int s = tid + NT * u;
+      if (s < NSLOTS) *(uint4*)(lds + (s / SLOTS_PER_ROW) * L::STRIDE + (s % SLOTS_PER_ROW) * 8) = v[u];
     }
     __syncthreads();
   }
@@ -69,38 +108,52 @@ __global__ __launch_bounds__(256) void k_quant_rows(const uint16_t* __restrict__
   v16f acc[RT];
 #pragma unroll
   for (int t = 0; t < RT; t++) acc[t] = v16f{};
+  FT_LDS uint16_t* xt = (FT_LDS uint16_t*)lds + L::PROJ_HW + wave * L::X_HW;  // this wave's 32x64 tile
+  const int r32 = lane & 31, h = lane >> 5;
 
-#pragma unroll 1
-  for (int i = 0; i < QR_CW / 64; i++) {
-    if (2 * i >= nblk) break;  // uniform across the workgroup
-    const int kb = 2 * i + h;
-    const bool ok = row_ok && kb < nblk;
-    uint32_t w[16];
-    if (ok) {
-      const uint4* p = (const uint4*)(src + (size_t)row * cols + c0 + kb * 32);
 #pragma unroll
-      for (int q = 0; q < 4; q++) {
-        uint4 v = load_nt16(p + q);
-        w[4 * q + 0] = v.x; w[4 * q + 1] = v.y; w[4 * q + 2] = v.z; w[4 * q + 3] = v.w;
+  for (int st = 0; st < NST; st++) {
+    if (2 * st >= nblk) break;  // uniform across the workgroup
+    if (st + PF < NST) issue(st + PF);
+    const int blk = 2 * st + (lane >> 2 & 1);           // this lane's block within the chunk
+    const bool col_ok = blk < nblk;
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+      const int row = rw0 + 8 * q + lr;
+      const bool ok = col_ok && row < rows;
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; e++) w[e] = ok ? (uint32_t)xv[st][q][e] : 0u;
+      uint32_t m = 0;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        const uint32_t a = w[e] & 0x7FFF7FFFu;
+        m = max(m, max(a & 0xFFFFu, a >> 16));
       }
-      uint32_t out[4];
-      const uint32_t sc = quantize32(w, out);
-      *(uint4*)(codes + (size_t)row * (cols >> 1) + ((c0 + kb * 32) >> 1)) = make_uint4(out[0], out[1], out[2], out[3]);
-      scales[(size_t)row * nbc + (c0 >> 5) + kb] = (uint8_t)sc;
-    } else {
-#pragma unroll
-      for (int q = 0; q < 16; q++) w[q] = 0;
+      m = quad_max(m);
+      const uint32_t code = e8m0_from_amax_bits(m);
+      const float s = e8m0_to_f32(code);
+      uint32_t o = 0;
+      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[0]), s, 0);
+      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[1]), s, 1);
+      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[2]), s, 2);
+      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[3]), s, 3);
+      if (ok) {
+        const int col = c0 + 64 * st + lc;
+        *(uint32_t*)(codes + (size_t)row * (cols >> 1) + (col >> 1)) = o;
+        if ((lane & 3) == 0) scales[(size_t)row * nbc + (col >> 5)] = (uint8_t)code;
+      }
+      if constexpr (MODE != 0) {
+        *(FT_LDS v4i*)(xt + (8 * q + lr) * QR_XSTRIDE + lc) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+      }
     }
 
     if constexpr (MODE != 0) {
       const int g16 = lane >> 4, t16 = lane & 15;
 #pragma unroll
-      for (int q = 0; q < 4; q++) {
-        uint32_t ah[8];
-#pragma unroll
-        for (int e = 0; e < 4; e++) { ah[2 * e] = w[4 * q + e] & 0xFFFFu; ah[2 * e + 1] = w[4 * q + e] >> 16; }
-        const v8bf a = pack_v8bf(ah);
-        const int kloc = kb * 32 + 8 * q;  // chunk position of this lane's 8 elements
+      for (int kk = 0; kk < 4; kk++) {
+        const v8bf a = __builtin_bit_cast(v8bf, *(const FT_LDS v4i*)(xt + r32 * QR_XSTRIDE + 16 * kk + 8 * h));
+        const int kloc = 64 * st + 16 * kk + 8 * h;  // chunk position of this lane's 8 elements
 #pragma unroll
         for (int t = 0; t < RT; t++) {
           v8bf b;
@@ -123,14 +176,13 @@ __global__ __launch_bounds__(256) void k_quant_rows(const uint16_t* __restrict__
   }
 
   if constexpr (MODE != 0) {
-    const int rbase = blockIdx.x * QR_ROWS + wave * 32;
 #pragma unroll
     for (int t = 0; t < RT; t++) {
       const int j = t * 32 + r32;
       if (j >= R) continue;
 #pragma unroll
       for (int v = 0; v < 16; v++) {
-        const int rr = rbase + 8 * (v >> 2) + 4 * h + (v & 3);
+        const int rr = rw0 + 8 * (v >> 2) + 4 * h + (v & 3);
         if (rr < rows) {
           float* dst = proj_out + (size_t)rr * R + j;
           if (use_atomics) atomicAdd(dst, acc[t][v]);
@@ -178,45 +230,49 @@ __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict_
   if (lane == 0) scales[(size_t)tr * nbc + tc] = (uint8_t)code;
 }
 
+// Fill with 16-byte stores (p is 16-byte aligned); the last n % 4 floats singly.
 __global__ void k_fill_f32(float* __restrict__ p, size_t n, float v) {
+  const size_t n4 = n >> 2;
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t st = (size_t)gridDim.x * blockDim.x;
-  for (; i < n; i += st) p[i] = v;
+  for (size_t j = i; j < n4; j += st) ((float4*)p)[j] = make_float4(v, v, v, v);
+  if (i < (n & 3)) p[4 * n4 + i] = v;
 }
 
 // ---------------------------------------------------------------- launchers
-template <int RT, int MODE>
+template <int RT, int MODE, int WAVES, int CW>
 static hipError_t launch_rows_t(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
                                 const uint16_t* proj, int R, float* proj_out, hipStream_t st) {
-  dim3 grid((rows + QR_ROWS - 1) / QR_ROWS, (cols + QR_CW - 1) / QR_CW);
+  dim3 grid((rows + 32 * WAVES - 1) / (32 * WAVES), (cols + CW - 1) / CW);
   const int atomics = MODE != 0 && grid.y > 1;
   if (atomics) {
-    const size_t n = (size_t)rows * R;
-    k_fill_f32<<<(unsigned)std::min<size_t>((n + 255) / 256, 4096), 256, 0, st>>>(proj_out, n, 0.0f);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_fill_f32(proj_out, (size_t)rows * R, 0.0f, st);
     if (e != hipSuccess) return e;
   }
-  k_quant_rows<RT, MODE><<<grid, 256, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, atomics);
+  k_quant_rows<RT, MODE, WAVES, CW><<<grid, 64 * WAVES, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, atomics);
   return hipGetLastError();
 }
 
+// Geometry per mode, from timing at the FLUX shapes: 8 waves (256 rows) per
+// workgroup amortize the staged projection chunk; the [R, cols] projection
+// takes 768-column chunks (fewer atomic partial sums) while the chunk fits LDS.
 hipError_t launch_quant_rows(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
                              const uint16_t* proj, int R, int layout, float* proj_out, hipStream_t st) {
-  if (!proj || R == 0) return launch_rows_t<1, 0>(src, rows, cols, codes, scales, nullptr, 0, nullptr, st);
+  if (!proj || R == 0) return launch_rows_t<1, 0, 4, 384>(src, rows, cols, codes, scales, nullptr, 0, nullptr, st);
   const int rt = (R + 31) / 32;
   if (layout == 0) {
     switch (rt) {
-      case 1: return launch_rows_t<1, 1>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-      case 2: return launch_rows_t<2, 1>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-      case 3: return launch_rows_t<3, 1>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-      default: return launch_rows_t<4, 1>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+      case 1: return launch_rows_t<1, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+      case 2: return launch_rows_t<2, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+      case 3: return launch_rows_t<3, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+      default: return launch_rows_t<4, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
     }
   }
   switch (rt) {
-    case 1: return launch_rows_t<1, 2>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-    case 2: return launch_rows_t<2, 2>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-    case 3: return launch_rows_t<3, 2>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-    default: return launch_rows_t<4, 2>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+    case 1: return launch_rows_t<1, 2, 8, 768>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+    case 2: return launch_rows_t<2, 2, 8, 768>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+    case 3: return launch_rows_t<3, 2, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+    default: return launch_rows_t<4, 2, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
   }
 }
 
@@ -229,7 +285,7 @@ hipError_t launch_quant_tiles(const uint16_t* src, int rows, int cols, uint8_t* 
 
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st) {
   if (n == 0) return hipSuccess;
-  k_fill_f32<<<(unsigned)std::min<size_t>((n + 255) / 256, 4096), 256, 0, st>>>(p, n, v);
+  k_fill_f32<<<(unsigned)std::min<size_t>((n / 4 + 255) / 256 + 1, 2048), 256, 0, st>>>(p, n, v);
   return hipGetLastError();
 }
 

@@ -112,3 +112,6 @@ def test_lora_validation():
     assert f(*args(dA=NULL)) == _lib.FT_ERR_NULL
     assert f(*args(x=NULL)) == _lib.FT_ERR_NULL
     assert f(*args(dy=MISALIGNED)) == _lib.FT_ERR_ALIGN
+    assert f(*args(xa=MISALIGNED)) == _lib.FT_ERR_ALIGN
+    assert f(*args(dyb=MISALIGNED)) == _lib.FT_ERR_ALIGN
+    assert f(*args(N=(1 << 24) + 32)) == _lib.FT_ERR_UNSUPPORTED

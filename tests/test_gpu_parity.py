@@ -24,7 +24,7 @@ from tests._helpers import adversarial_rows, f64, random_rows
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-QR_CW = 384  # column chunk of the fused quantize kernel (partial sums combine per chunk)
+QR_CW = 384  # narrowest column chunk of the fused quantize kernel (fp32 partial sums combine per chunk)
 
 
 def dev_bf16(bits):
@@ -203,6 +203,32 @@ def test_lora_grads_accumulate():
     # atomics combine partial sums in any order: compare in norm, not per element
     assert torch.linalg.norm(dA2 - 2 * dA) <= 1e-5 * torch.linalg.norm(dA)
     assert torch.linalg.norm(dB2 - 2 * dB) <= 1e-5 * torch.linalg.norm(dB)
+
+
+@pytest.mark.parametrize("M,K,N,r,ld", [(1, 32, 32, 1, 4), (100, 160, 96, 8, 8), (700, 416, 1312, 40, 64),
+                                        (257, 3072, 288, 96, 96), (130, 256, 544, 128, 128),
+                                        (513, 1184, 2080, 32, 64)])
+def test_lora_grads_shapes(M, K, N, r, ld):
+    """Adapter gradients with fp32 factors given directly: every rank tile
+    count, row strides above r, column counts that leave partial 128-column
+    groups and token counts that leave partial 64-row stages."""
+    rng = np.random.default_rng(M + K + r)
+    X = gen.f32_to_bf16_bits(rng.standard_normal((M, K)).astype(np.float32))
+    dY = gen.f32_to_bf16_bits((1e-3 * rng.standard_t(3, (M, N))).astype(np.float32))
+    xa = np.zeros((M, ld), np.float32)
+    gbt = np.zeros((M, ld), np.float32)
+    xa[:, :r] = rng.standard_normal((M, r)).astype(np.float32)
+    gbt[:, :r] = (1e-3 * rng.standard_normal((M, r))).astype(np.float32)
+    xa[:, r:] = np.float32(7.0)   # columns past r must not reach the outputs
+    gbt[:, r:] = np.float32(-5.0)
+    dA, dB = _lib.ft_lora_grads(dev_bf16(X), dev_bf16(dY), torch.from_numpy(xa).to(DEV),
+                                torch.from_numpy(gbt).to(DEV), r, col0=0)
+    torch.cuda.synchronize()
+    dAr, dBr, _, _ = ref.lora_grads(X, dY, xa[:, :r].astype(np.float64), gbt[:, :r].astype(np.float64),
+                                    want_s=False)
+    assert host(dA).shape == (K, r) and host(dB).shape == (r, N)
+    assert np.linalg.norm(host(dA) - dAr) <= 1e-3 * np.linalg.norm(dAr)
+    assert np.linalg.norm(host(dB) - dBr) <= 1e-3 * np.linalg.norm(dBr)
 
 
 def test_gemm_random_codes():
