@@ -27,6 +27,7 @@ typedef short v4s __attribute__((ext_vector_type(4)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+typedef float v2f __attribute__((ext_vector_type(2)));
 
 #define FT_LDS __attribute__((address_space(3)))
 
@@ -173,13 +174,17 @@ __device__ __forceinline__ void wait_vm() {
 // barrier.  lds_base must be wave-uniform.
 // The byte offset is voff (per lane) + soff (uniform); a voff at or beyond the
 // buffer size reads zeros whatever soff is.
+// The uniform operands pass through readfirstlane: the compiler may hold a
+// uniform value in a VGPR, which an "s" asm operand would not convert.
 __device__ __forceinline__ void dma16(v4i rsrc, uint32_t lds_base, uint32_t voff, uint32_t soff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               :: "s"(lds_base), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc),
+                  "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
 }
 __device__ __forceinline__ void dma4(v4i rsrc, uint32_t lds_base, uint32_t voff, uint32_t soff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
-               :: "s"(lds_base), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc),
+                  "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
 }
 
 }  // namespace ft

@@ -459,6 +459,23 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       }
     }
   };
+  // Single-fragment reads, for interleaving with the MFMAs one at a time.
+  // Fragment q of a k-step: q < 4 -> A row tile q; q >= 4 -> W tile q - 4
+  // (backward: its two transposing halves are fragments 4 + 2j and 5 + 2j).
+  constexpr int FRAG_READS = BWD ? 12 : 8;
+  auto read_one = [&](int t, int kk, int q, Fp4Frag& f) {
+    const uint8_t* slot = lds + slot_of(t);
+    if (q < 4) {
+      f.a[q] = *(const v4i*)(slot + rd_a[kk] + q * 32 * PROW);
+    } else if constexpr (!BWD) {
+      f.b[q - 4] = *(const v4i*)(slot + rd_b[kk] + (q - 4) * 32 * PROW);
+    } else {
+      const int j = (q - 4) >> 1, half = (q - 4) & 1;
+      const v2i v = lds_read_tr4((const FT_LDS void*)(slot + rd_t[kk][j] + half * 16 * 128));
+      if (half == 0) { f.b[j][0] = v[0]; f.b[j][1] = v[1]; }
+      else { f.b[j][2] = v[0]; f.b[j][3] = v[1]; }
+    }
+  };
   // Raw scale words of a stage; turned into MFMA scale operands (one byte per
   // k-step) only when the stage's MFMAs are about to issue.
   struct ScaleRaw { uint32_t a[4], b[4]; };
@@ -515,11 +532,21 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     }
   };
 
+  // Accumulators start at the bias (forward): every output column's sum then
+  // begins with its bias term, in both output precisions.
   v16f acc[4][4];
 #pragma unroll
-  for (int i = 0; i < 4; i++)
+  for (int j = 0; j < 4; j++) {
+    float b0 = 0.f;
+    if constexpr (!BWD) {
+      const int gc = n0 + wn * 128 + j * 32 + r32;
+      if (bias && gc < N) b0 = bf16_to_f32(bias[gc]);
+    }
 #pragma unroll
-    for (int j = 0; j < 4; j++) acc[i][j] = v16f{};
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+      for (int v = 0; v < 16; v++) acc[i][j][v] = b0;
+  }
 
   auto mfma_fp4_step = [&](int kk, const Fp4Frag& f, const uint32_t (&sa)[4], const uint32_t (&sb)[4]) {
 #pragma unroll
@@ -565,40 +592,98 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   read_scales(0, sr);
 
   // One FP4 iteration.  STEADY: stages t+1..t+3 are FP4 stages, so the body is
-  // branch-free with constant wait counts (no register copies of fragments).
-  auto fp4_iter = [&](int t, auto steady) {
-    constexpr bool S = decltype(steady)::value;
-    uint32_t sa[4], sb[4];
-    scale_ops(sr, sa, sb);               // reads issued a k-step ago: f0 and this stage's scales
+  // branch-free with constant wait counts, and every other instruction is
+  // placed between two MFMAs (one wave per SIMD: the matrix pipe only stays
+  // busy if nothing else waits in front of the next MFMA):
+  //   k-step 0 (16 MFMAs on f0) carries the reads of this stage's k-step 1;
+  //   then the barrier that publishes stage t+1;
+  //   k-step 1 (16 MFMAs on f1) carries the reads of stage t+1's k-step 0 and
+  //   scales, the loads of stage t+3, and the scale operands of stage t+1.
+  uint32_t sa[4], sb[4];
+  scale_ops(sr, sa, sb);
+  auto fp4_iter_steady = [&](int t) {
+    const uint8_t* nslot = lds + slot_of(t + 1);
+    const uint32_t dslot = lds0 + slot_of(t + 3);
+    const uint32_t a_off = (uint32_t)(t + 3) * PROW;
+    const uint32_t wt_off = (uint32_t)(t + 3) * PK * ldw;
+    const uint32_t s_off = (uint32_t)(t + 3) * 4;
     __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int m = 0; m < 16; m++) {
+      const int i = m >> 2, j = m & 3;
+      acc[i][j] = mfma_fp4_32x32x64<0>(f0.a[i], f0.b[j], acc[i][j], (int)sa[i], (int)sb[j]);
+      if (m < FRAG_READS) read_one(t, 1, m, f1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    wait_vm<LOADS_FP4>();                // stage t+1 landed; stage t+2 may stay in flight
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    uint32_t nsa[4], nsb[4];
+#pragma unroll
+    for (int m = 0; m < 16; m++) {
+      const int i = m >> 2, j = m & 3;
+      acc[i][j] = mfma_fp4_32x32x64<1>(f1.a[i], f1.b[j], acc[i][j], (int)sa[i], (int)sb[j]);
+      // reads of stage t+1: fragments in slots 0..FRAG_READS-1, then scales
+      if (m < FRAG_READS) read_one(t + 1, 0, m, f0);
+      if (m == FRAG_READS - 4 || (BWD && m == 12)) {
+        if (m == FRAG_READS - 4) {
+#pragma unroll
+          for (int q = 0; q < 4; q++) sr.a[q] = *(const uint32_t*)(nslot + rd_sa + q * 128);
+        }
+        if (!BWD || m == 12) {
+          if constexpr (!BWD) {
+#pragma unroll
+            for (int q = 0; q < 4; q++)
+              sr.b[q] = *(const uint32_t*)(nslot + OFF_SB + (wn * 2 + (q >> 1)) * 256 + (q & 1) * 4);
+          } else {
+            sr.b[0] = *(const uint32_t*)(nslot + rd_sbt);
+            sr.b[1] = *(const uint32_t*)(nslot + rd_sbt + 512);
+          }
+        }
+      }
+      // loads of stage t+3: A tile rows in slots 0..3, W tile in 4..7, scales in 8, 9
+      if (m < 4) dma16(ra, dslot + (wave * 64 + 16 * m) * PROW, a_base[m], a_off);
+      else if (m < 8) {
+        if constexpr (!BWD) dma16(rw, dslot + OFF_B + (wave * 64 + 16 * (m - 4)) * PROW, w_base[m - 4], a_off);
+        else dma16(rw, dslot + OFF_B + (wave * 32 + 8 * (m - 4)) * 128, wt_base[m - 4], wt_off);
+      } else if (m == 8) {
+        dma4(ras, dslot + OFF_SA + wave * 256, sa_base, s_off);
+      } else if (m == 9) {
+        if constexpr (!BWD) dma4(rws, dslot + OFF_SB + wave * 256, sb_base, s_off);
+        else dma4(rws, dslot + OFF_SB + wave * 256, sb_base, s_off * nwkb);
+      }
+      // scale operands of stage t+1 once its scale words are in registers
+      if (m == 15) scale_ops(sr, nsa, nsb);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; q++) { sa[q] = nsa[q]; sb[q] = nsb[q]; }
+  };
+
+  // Remaining FP4 iterations (the last three stages): loads may run out, so
+  // waits and issues follow the stage kinds.
+  auto fp4_iter = [&](int t) {
     read_fp4(t, 1, f1);
     __builtin_amdgcn_sched_barrier(0);
     mfma_fp4_step(0, f0, sa, sb);
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (S) {
-      wait_vm<LOADS_FP4>();              // stage t+1 landed; stage t+2 may stay in flight
-      __builtin_amdgcn_s_barrier();
-      asm volatile("" ::: "memory");
-      issue_fp4(t + 3);                  // into the slot of stage t-1
+    publish(loads_of(t + 2));
+    issue(t + 3);
+    if (t + 1 < nst) {
       read_fp4(t + 1, 0, f0);
       read_scales(t + 1, sr);
-    } else {
-      publish(loads_of(t + 2));
-      issue(t + 3);
-      if (t + 1 < nst) {
-        read_fp4(t + 1, 0, f0);
-        read_scales(t + 1, sr);
-      }
     }
     __builtin_amdgcn_sched_barrier(0);
     mfma_fp4_step(1, f1, sa, sb);
     __builtin_amdgcn_sched_barrier(0);
+    if (t + 1 < nst) scale_ops(sr, sa, sb);
   };
   int t = 0;
 #pragma unroll 1
-  for (; t + 3 < nst; t++) fp4_iter(t, std::true_type{});
+  for (; t + 3 < nst; t++) fp4_iter_steady(t);
 #pragma unroll 1
-  for (; t < nst; t++) fp4_iter(t, std::false_type{});
+  for (; t < nst; t++) fp4_iter(t);
   if (nlr > 0) {
     LrFrag g;
     read_lr(nst, g);
@@ -616,17 +701,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     }
   }
 
-  // ---------------- epilogue: bias, convert, store
-  float bb[4] = {0.f, 0.f, 0.f, 0.f};
-  if constexpr (!BWD) {
-    if (bias) {
-#pragma unroll
-      for (int j = 0; j < 4; j++) {
-        const int gc = n0 + wn * 128 + j * 32 + r32;
-        bb[j] = gc < NO ? bf16_to_f32(bias[gc]) : 0.f;
-      }
-    }
-  }
+  // ---------------- epilogue: convert, store
   if constexpr (OUT_F32) {
 #pragma unroll
     for (int j = 0; j < 4; j++) {
@@ -637,32 +712,44 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
 #pragma unroll
         for (int v = 0; v < 16; v++) {
           const int gr = m0 + wm * 128 + i * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-          if (gr < M) ((float*)out)[(size_t)gr * NO + gc] = acc[i][j][v] + bb[j];
+          if (gr < M) ((float*)out)[(size_t)gr * NO + gc] = acc[i][j][v];
         }
     }
   } else {
-    // each wave stages its 128x128 bf16 sub-tile (row stride 272 bytes) and
-    // writes it back as 16-byte row segments
+    // Each wave stages its 128x128 sub-tile in LDS column by column (a lane's
+    // four consecutive rows of one column are one 8-byte write, converted in
+    // pairs), then reads it back row-major with the transposing 16-bit read:
+    // source lane s of a 16-lane group reads 4 rows of column
+    // cb + 8(s%4) + s/4 (+4 in the second read), so output lane i holds
+    // columns cb + 8(i/4) .. +7 of row rb + i%4 and stores them as 16 bytes.
     __syncthreads();  // all waves are done with the ring
-    constexpr int OS = 128 * 2 + 16;
-    uint8_t* ow = lds + wave * (128 * OS);
+    constexpr int CS = 128 * 2 + 8;   // bytes per staged column
+    uint8_t* ow = lds + wave * (128 * CS);
 #pragma unroll
     for (int i = 0; i < 4; i++)
 #pragma unroll
       for (int j = 0; j < 4; j++)
 #pragma unroll
-        for (int v = 0; v < 16; v++) {
-          const int rr = i * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-          const int cc = j * 32 + r32;
-          *(uint16_t*)(ow + rr * OS + cc * 2) = (uint16_t)f32_to_bf16_rne(acc[i][j][v] + bb[j]);
+        for (int q = 0; q < 4; q++) {
+          const int rr = i * 32 + 8 * q + 4 * h, cc = j * 32 + r32;
+          const v2f x01 = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]};
+          const v2f x23 = {acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          const v2i w = {(int)__builtin_bit_cast(uint32_t, __builtin_convertvector(x01, v2bf)),
+                         (int)__builtin_bit_cast(uint32_t, __builtin_convertvector(x23, v2bf))};
+          *(v2i*)(ow + cc * CS + rr * 2) = w;
         }
-    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // the wave reads back only its own area
+    const int src_col = 8 * (t16 & 3) + (t16 >> 2);
 #pragma unroll
     for (int it = 0; it < 32; it++) {
-      const int rr = it * 4 + (lane >> 4), cc = (lane & 15) * 8;
-      const int gr = m0 + wm * 128 + rr, gc = n0 + wn * 128 + cc;
-      const uint4 v = *(const uint4*)(ow + rr * OS + cc * 2);
-      if (gr < M && gc < NO) *(uint4*)((uint16_t*)out + (size_t)gr * NO + gc) = v;
+      const int cb = 32 * (it & 3), rb = 16 * (it >> 2) + 4 * g16;
+      const FT_LDS uint8_t* p = (const FT_LDS uint8_t*)ow + (cb + src_col) * CS + rb * 2;
+      const v4s lo = lds_read_tr16(p), hi = lds_read_tr16(p + 4 * CS);
+      const int gr = m0 + wm * 128 + rb + (t16 & 3), gc = n0 + wn * 128 + cb + 8 * (t16 >> 2);
+      if (gr < M && gc < NO)
+        *(v4i*)((uint16_t*)out + (size_t)gr * NO + gc) =
+            v4i{(int)(((uint32_t)(uint16_t)lo[1] << 16) | (uint16_t)lo[0]), (int)(((uint32_t)(uint16_t)lo[3] << 16) | (uint16_t)lo[2]),
+                (int)(((uint32_t)(uint16_t)hi[1] << 16) | (uint16_t)hi[0]), (int)(((uint32_t)(uint16_t)hi[3] << 16) | (uint16_t)hi[2])};
     }
   }
 }
