@@ -129,6 +129,11 @@ def main():
     Qp = torch.empty((M, R), dtype=f32, device=dev)
     dX = torch.empty((M, K), dtype=bf, device=dev)
     dA = torch.empty((K, r), dtype=f32, device=dev); dB = torch.empty((r, N), dtype=f32, device=dev)
+    # workspaces for the partial sums (allocated once, outside the timed region)
+    wspace = lambda n: torch.empty(max(n, 16), dtype=u8, device=dev)
+    ws_x = wspace(_lib.ft_quantize_workspace_size(M, K, 1, R, _lib.FT_PROJ_COLS_BY_R))
+    ws_dy = wspace(_lib.ft_quantize_workspace_size(M, N, 1, R, _lib.FT_PROJ_R_BY_COLS))
+    ws_lg = wspace(_lib.ft_lora_grads_workspace_size(M, K, N, R, r))
 
     names = ["quantize_x", "gemm_fwd", "quantize_dy", "gemm_bwd", "lora_grads"]
 
@@ -137,15 +142,17 @@ def main():
             if ev is not None:
                 ev[i].record()
         mark(0)
-        _lib.ft_quantize_blockwise(X, proj=D, proj_layout=_lib.FT_PROJ_COLS_BY_R, codes=xq, scales=xs, proj_out=P)
+        _lib.ft_quantize_blockwise(X, proj=D, proj_layout=_lib.FT_PROJ_COLS_BY_R, codes=xq, scales=xs, proj_out=P,
+                                   workspace=ws_x)
         mark(1)
         _lib.ft_linear_fwd(xq, xs, wq, ws, K, P, U, bias, y=Y)
         mark(2)
-        _lib.ft_quantize_blockwise(dY, proj=U, proj_layout=_lib.FT_PROJ_R_BY_COLS, codes=gq, scales=gs, proj_out=Qp)
+        _lib.ft_quantize_blockwise(dY, proj=U, proj_layout=_lib.FT_PROJ_R_BY_COLS, codes=gq, scales=gs, proj_out=Qp,
+                                   workspace=ws_dy)
         mark(3)
         _lib.ft_linear_bwd_input(gq, gs, wq, ws, K, Qp, D, dx=dX)
         mark(4)
-        _lib.ft_lora_grads(X, dY, P, Qp, r, col0=rs, dA=dA, dB=dB)
+        _lib.ft_lora_grads(X, dY, P, Qp, r, col0=rs, dA=dA, dB=dB, workspace=ws_lg)
         mark(5)
 
     for _ in range(args.warmup):

@@ -85,15 +85,25 @@ typedef enum ft_proj_layout {
  *              U = [L2;B]).  Only with block_rows == 1.
  *   R          0 when proj is NULL; else 16 <= R <= 128 and R % 16 == 0.
  *   proj_out   fp32 [rows, R] = src . proj (or src . proj^T), products of the
- *              unquantized bf16 inputs with fp32 accumulation.  Partial sums
- *              over column chunks are combined with atomic adds, so the last
- *              bit may vary between runs.
+ *              unquantized bf16 inputs with fp32 accumulation.  Column chunks
+ *              of the row leave fp32 partial sums in the workspace, which a
+ *              second kernel adds in a fixed order (results are reproducible).
+ *   workspace  device memory of at least ft_quantize_workspace_size(...) bytes,
+ *              16-byte aligned, owned by the caller; contents on entry are
+ *              ignored and on return undefined.  May be NULL when the size is
+ *              0 (no projection, or the columns fit one chunk).  Calls that
+ *              share a workspace must not overlap.
  * rows == 0 is a no-op.  rows < 2^31, cols < 2^31.
  */
 ft_status ft_quantize_blockwise(const void *src, int64_t rows, int64_t cols, int32_t block_rows,
                                 uint8_t *codes, uint8_t *scales,
                                 const void *proj, int32_t R, ft_proj_layout proj_layout,
-                                float *proj_out, hipStream_t stream);
+                                float *proj_out, void *workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
+/* Workspace bytes ft_quantize_blockwise needs for these arguments (0: none). */
+size_t ft_quantize_workspace_size(int64_t rows, int64_t cols, int32_t block_rows, int32_t R,
+                                  ft_proj_layout proj_layout);
 
 /*
  * Forward of the triple-branch linear, Eq. (2), in nn.Linear orientation:
@@ -148,12 +158,21 @@ ft_status ft_linear_bwd_input(const uint8_t *gq, const uint8_t *gs, int64_t M, i
  *   r        1 <= r <= 128.
  *   dA       fp32 [K, r];  dB: fp32 [r, N].
  *   accumulate  0: overwrite dA and dB;  1: add into them.
- * Sums over M are combined across workgroups with atomic adds (last-bit
- * run-to-run variation).  K, N multiples of 32 and at most 2^24; M >= 0.
+ *   workspace  at least ft_lora_grads_workspace_size(M, K, N, ld, r) bytes,
+ *            16-byte aligned (NULL when that size is 0): token chunks leave
+ *            fp32 partial sums there and a second kernel adds them in a fixed
+ *            order (results are reproducible).  Calls sharing a workspace
+ *            must not overlap.
+ * K, N multiples of 32 and at most 2^24; M >= 0 (M == 0 gives zeros, or
+ * leaves dA and dB unchanged when accumulating).
  */
 ft_status ft_lora_grads(const void *x, int64_t M, int64_t K, const void *dy, int64_t N,
                         const float *xa, const float *dyb, int64_t ld, int32_t r,
-                        float *dA, float *dB, int32_t accumulate, hipStream_t stream);
+                        float *dA, float *dB, int32_t accumulate,
+                        void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes ft_lora_grads needs for these arguments (0: none). */
+size_t ft_lora_grads_workspace_size(int64_t M, int64_t K, int64_t N, int64_t ld, int32_t r);
 
 /* Static description of a status code. */
 const char *ft_status_string(ft_status status);

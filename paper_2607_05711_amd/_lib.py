@@ -43,10 +43,15 @@ def load():
                 "libfourtune.so is not built (expected at %s); run `python -m paper_2607_05711_amd.build` "
                 "or __graft_entry__.build()" % LIB_PATH)
         L = ctypes.CDLL(LIB_PATH)
-        L.ft_quantize_blockwise.argtypes = [_P, _I64, _I64, _I32, _P, _P, _P, _I32, ctypes.c_int, _P, _P]
+        _Z = ctypes.c_size_t
+        L.ft_quantize_blockwise.argtypes = [_P, _I64, _I64, _I32, _P, _P, _P, _I32, ctypes.c_int, _P, _P, _Z, _P]
+        L.ft_quantize_workspace_size.argtypes = [_I64, _I64, _I32, _I32, ctypes.c_int]
+        L.ft_quantize_workspace_size.restype = _Z
         L.ft_linear_fwd.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P, _P, ctypes.c_int, _P]
         L.ft_linear_bwd_input.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P, ctypes.c_int, _P]
-        L.ft_lora_grads.argtypes = [_P, _I64, _I64, _P, _I64, _P, _P, _I64, _I32, _P, _P, _I32, _P]
+        L.ft_lora_grads.argtypes = [_P, _I64, _I64, _P, _I64, _P, _P, _I64, _I32, _P, _P, _I32, _P, _Z, _P]
+        L.ft_lora_grads_workspace_size.argtypes = [_I64, _I64, _I64, _I64, _I32]
+        L.ft_lora_grads_workspace_size.restype = _Z
         for f in ("ft_quantize_blockwise", "ft_linear_fwd", "ft_linear_bwd_input", "ft_lora_grads"):
             getattr(L, f).restype = ctypes.c_int
         L.ft_status_string.argtypes = [ctypes.c_int]
@@ -92,11 +97,28 @@ def _need(t, name, dtype, device=None, ndim=None):
     return t
 
 
+def _workspace(nbytes, dev, workspace):
+    """The caller's workspace (checked for size) or a new one of nbytes."""
+    if nbytes == 0:
+        return workspace
+    if workspace is None:
+        return torch.empty(((nbytes + 15) // 16) * 16, dtype=torch.uint8, device=dev)
+    if workspace.numel() * workspace.element_size() < nbytes:
+        raise ValueError("workspace of %d bytes, %d required" % (workspace.numel() * workspace.element_size(), nbytes))
+    return workspace
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
 def ft_quantize_blockwise(src, block_rows=1, proj=None, proj_layout=FT_PROJ_COLS_BY_R,
-                          codes=None, scales=None, proj_out=None):
+                          codes=None, scales=None, proj_out=None, workspace=None):
     """MXFP4-quantize bf16 src [rows, cols]; optionally fused down-projection.
 
     Returns (codes uint8 [rows, cols/2], scales uint8, proj_out fp32 [rows, R] or None).
+    `workspace` (device tensor) holds the projection's partial sums; one of the
+    size ft_quantize_workspace_size reports is made when it is not given.
     """
     L = load()
     _need(src, "src", torch.bfloat16, ndim=2)
@@ -124,9 +146,15 @@ def ft_quantize_blockwise(src, block_rows=1, proj=None, proj_layout=FT_PROJ_COLS
             raise ValueError("proj_out must be [%d, %d]" % (rows, R))
     else:
         proj_out = None
+    workspace = _workspace(L.ft_quantize_workspace_size(rows, cols, block_rows, R, proj_layout), dev, workspace)
     _check(L.ft_quantize_blockwise(_ptr(src), rows, cols, block_rows, _ptr(codes), _ptr(scales),
-                                   _ptr(proj), R, proj_layout, _ptr(proj_out), _stream(dev)))
+                                   _ptr(proj), R, proj_layout, _ptr(proj_out), _ptr(workspace), _nbytes(workspace),
+                                   _stream(dev)))
     return codes, scales, proj_out
+
+
+def ft_quantize_workspace_size(rows, cols, block_rows=1, R=0, proj_layout=FT_PROJ_COLS_BY_R):
+    return int(load().ft_quantize_workspace_size(rows, cols, block_rows, R, proj_layout))
 
 
 def ft_linear_fwd(xq, xs, wq, ws, K, P=None, U=None, bias=None, out_dtype=torch.bfloat16, y=None):
@@ -189,7 +217,11 @@ def ft_linear_bwd_input(gq, gs, wq, ws, K, Qp=None, D=None, out_dtype=torch.bflo
     return dx
 
 
-def ft_lora_grads(x, dy, xa, dyb, r, col0=0, dA=None, dB=None, accumulate=False):
+def ft_lora_grads_workspace_size(M, K, N, ld, r):
+    return int(load().ft_lora_grads_workspace_size(M, K, N, ld, r))
+
+
+def ft_lora_grads(x, dy, xa, dyb, r, col0=0, dA=None, dB=None, accumulate=False, workspace=None):
     """dA = x^T dyb[:, col0:col0+r] [K, r];  dB = xa[:, col0:col0+r]^T dy [r, N].
 
     xa and dyb are contiguous fp32 [M, ld] (normally P and Qp, with the adapter
@@ -214,6 +246,8 @@ def ft_lora_grads(x, dy, xa, dyb, r, col0=0, dA=None, dB=None, accumulate=False)
     _need(dB, "dB", torch.float32, dev)
     if dA.shape != (K, r) or dB.shape != (r, N):
         raise ValueError("dA must be [K, r] and dB [r, N]")
+    workspace = _workspace(L.ft_lora_grads_workspace_size(M, K, N, ld, r), dev, workspace)
     _check(L.ft_lora_grads(_ptr(x), M, K, _ptr(dy), N, _ptr(xa, col0), _ptr(dyb, col0), ld, r,
-                           _ptr(dA), _ptr(dB), 1 if accumulate else 0, _stream(dev)))
+                           _ptr(dA), _ptr(dB), 1 if accumulate else 0, _ptr(workspace), _nbytes(workspace),
+                           _stream(dev)))
     return dA, dB

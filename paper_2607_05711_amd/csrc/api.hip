@@ -45,6 +45,14 @@ ft_status check_rank(int32_t R, const void* a, const void* b, const char* an, co
   return FT_OK;
 }
 
+ft_status check_workspace(const void* ws, size_t bytes, size_t need) {
+  if (need == 0) return FT_OK;
+  if (!ws) return fail(FT_ERR_NULL, "a workspace of %zu bytes is required", need);
+  if (bytes < need) return fail(FT_ERR_SHAPE, "workspace of %zu bytes, %zu required", bytes, need);
+  if (!aligned16(ws)) return fail(FT_ERR_ALIGN, "workspace not 16-byte aligned");
+  return FT_OK;
+}
+
 #define FT_TRY(x)                   \
   do {                              \
     ft_status s_ = (x);             \
@@ -69,9 +77,15 @@ const char* ft_status_string(ft_status s) {
 
 const char* ft_last_error(void) { return g_last_error; }
 
+size_t ft_quantize_workspace_size(int64_t rows, int64_t cols, int32_t block_rows, int32_t R,
+                                  ft_proj_layout proj_layout) {
+  if (block_rows != 1 || R <= 0 || R > 128 || rows <= 0 || cols <= 0 || rows > kMaxDim || cols > kMaxDim) return 0;
+  return ft::quant_rows_workspace((int)rows, (int)cols, R, (int)proj_layout);
+}
+
 ft_status ft_quantize_blockwise(const void* src, int64_t rows, int64_t cols, int32_t block_rows, uint8_t* codes,
                                 uint8_t* scales, const void* proj, int32_t R, ft_proj_layout proj_layout,
-                                float* proj_out, hipStream_t stream) {
+                                float* proj_out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   g_last_error[0] = 0;
   FT_TRY(check_dim("rows", rows, block_rows == 32 ? 32 : 1));
   FT_TRY(check_dim("cols", cols, 32));
@@ -87,8 +101,11 @@ ft_status ft_quantize_blockwise(const void* src, int64_t rows, int64_t cols, int
     return hip_status(ft::launch_quant_tiles((const uint16_t*)src, (int)rows, (int)cols, codes, scales, stream),
                       "quantize 32x32");
   }
+  FT_TRY(check_workspace(workspace, workspace_bytes,
+                         R ? ft::quant_rows_workspace((int)rows, (int)cols, R, (int)proj_layout) : 0));
   return hip_status(ft::launch_quant_rows((const uint16_t*)src, (int)rows, (int)cols, codes, scales,
-                                          (const uint16_t*)proj, R, (int)proj_layout, proj_out, stream),
+                                          (const uint16_t*)proj, R, (int)proj_layout, proj_out, (float*)workspace,
+                                          stream),
                     "quantize 1x32");
 }
 
@@ -129,9 +146,16 @@ ft_status ft_linear_bwd_input(const uint8_t* gq, const uint8_t* gs, int64_t M, i
                     "linear bwd input");
 }
 
+size_t ft_lora_grads_workspace_size(int64_t M, int64_t K, int64_t N, int64_t ld, int32_t r) {
+  if (M <= 0 || K <= 0 || N <= 0 || r < 1 || r > 128 || ld < r || M > kMaxDim || K > (1 << 24) || N > (1 << 24) ||
+      ld > 4096)
+    return 0;
+  return ft::lora_grads_workspace((int)M, (int)K, (int)N, (int)ld, r);
+}
+
 ft_status ft_lora_grads(const void* x, int64_t M, int64_t K, const void* dy, int64_t N, const float* xa,
                         const float* dyb, int64_t ld, int32_t r, float* dA, float* dB, int32_t accumulate,
-                        hipStream_t stream) {
+                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
   g_last_error[0] = 0;
   FT_TRY(check_dim("M", M, 1));
   FT_TRY(check_dim("K", K, 32));
@@ -145,8 +169,9 @@ ft_status ft_lora_grads(const void* x, int64_t M, int64_t K, const void* dy, int
   if ((x && !aligned16(x)) || (dy && !aligned16(dy)) || (xa && !aligned16(xa)) || (dyb && !aligned16(dyb)) ||
       !aligned16(dA) || !aligned16(dB))
     return fail(FT_ERR_ALIGN, "x, dy, xa, dyb, dA, dB must be 16-byte aligned");
+  FT_TRY(check_workspace(workspace, workspace_bytes, ft::lora_grads_workspace((int)M, (int)K, (int)N, (int)ld, r)));
   return hip_status(ft::launch_lora_grads((const uint16_t*)x, (int)M, (int)K, (const uint16_t*)dy, (int)N, xa, dyb,
-                                          (int)ld, r, dA, dB, accumulate != 0, stream),
+                                          (int)ld, r, dA, dB, accumulate != 0, (float*)workspace, stream),
                     "lora grads");
 }
 

@@ -46,6 +46,16 @@ __device__ __forceinline__ void split_bf16(float x, uint32_t& hi, uint32_t& lo) 
   lo = f32_to_bf16_rne(x - bf16_to_f32(hi));
 }
 
+// The same split for two values at once with the packed round-to-nearest-even
+// convert: hi and lo hold bf16 pairs (a in the low half, b in the high half).
+// x - hi is exact in fp32, so lo is the rounding of the true remainder.
+__device__ __forceinline__ void split_bf16x2(float a, float b, uint32_t& hi, uint32_t& lo) {
+  const v2f x = {a, b};
+  hi = __builtin_bit_cast(uint32_t, __builtin_convertvector(x, v2bf));
+  const v2f hf = {__uint_as_float(hi << 16), __uint_as_float(hi & 0xFFFF0000u)};
+  lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(x - hf, v2bf));
+}
+
 // E8M0 block scale from the largest |bf16| bit pattern of a block (sign
 // cleared): floor(log2 amax) - 2 + 127, clamped at 0.  A zero or subnormal
 // amax gives 0 (e = -127).

@@ -6,12 +6,19 @@
 
 namespace ft {
 
-
+// 1x32 row quantization with the fused down-projection.  When the columns
+// span several chunks, each chunk's fp32 projection partial goes to `ws`
+// (quant_rows_workspace bytes) and a reduction kernel sums them into
+// proj_out; otherwise proj_out is written directly and ws is unused.
+size_t quant_rows_workspace(int rows, int cols, int R, int layout);
 hipError_t launch_quant_rows(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
-                             const uint16_t* proj, int R, int layout, float* proj_out, hipStream_t st);
+                             const uint16_t* proj, int R, int layout, float* proj_out, float* ws, hipStream_t st);
 hipError_t launch_quant_tiles(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
                               hipStream_t st);
-hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st);
+
+// out0 (+)= sum of nparts partials [n0 | n1] in ws; likewise out1.  n0, n1 multiples of 4.
+hipError_t launch_reduce_parts(const float* ws, int nparts, size_t n0, float* out0, size_t n1, float* out1,
+                               bool accumulate, hipStream_t st);
 
 // FP4 GEMM.  bwd = false: out[M, N] = A[M, K] . W[N, K]^T  (+ P . U + bias)
 //            bwd = true : out[M, K] = A[M, N] . W[N, K]    (+ P . D^T)
@@ -19,8 +26,10 @@ hipError_t launch_gemm_fp4(bool bwd, const uint8_t* a, const uint8_t* as, const 
                            int M, int N, int K, const float* P, int R, const uint16_t* lr,
                            const uint16_t* bias, void* out, bool out_f32, hipStream_t st);
 
+// Adapter gradients; token chunks leave partials in ws (lora_grads_workspace bytes).
+size_t lora_grads_workspace(int M, int K, int N, int ld, int r);
 hipError_t launch_lora_grads(const uint16_t* x, int M, int K, const uint16_t* dy, int N, const float* xa,
-                             const float* dyb, int ld, int r, float* dA, float* dB, bool accumulate,
+                             const float* dyb, int ld, int r, float* dA, float* dB, bool accumulate, float* ws,
                              hipStream_t st);
 
 }  // namespace ft

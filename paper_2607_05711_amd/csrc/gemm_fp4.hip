@@ -307,6 +307,19 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
 
   const int nst = KR / PK, nlr = R / 16, total = nst + nlr;
 
+  // Bias of this lane's four output columns (forward), loaded first so its
+  // latency overlaps the first stage loads.
+  float bias4[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (!BWD) {
+    if (bias) {
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const int gc = n0 + wn * 128 + j * 32 + r32;
+        if (gc < N) bias4[j] = bf16_to_f32(bias[gc]);
+      }
+    }
+  }
+
   // ---------------- per-lane load geometry (constant over stages)
   // Each buffer load takes a per-lane byte offset (constant over stages; rows
   // outside the matrix hold kOobOffset, which reads zeros) plus a uniform
@@ -536,17 +549,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   // begins with its bias term, in both output precisions.
   v16f acc[4][4];
 #pragma unroll
-  for (int j = 0; j < 4; j++) {
-    float b0 = 0.f;
-    if constexpr (!BWD) {
-      const int gc = n0 + wn * 128 + j * 32 + r32;
-      if (bias && gc < N) b0 = bf16_to_f32(bias[gc]);
-    }
+  for (int j = 0; j < 4; j++)
 #pragma unroll
     for (int i = 0; i < 4; i++)
 #pragma unroll
-      for (int v = 0; v < 16; v++) acc[i][j][v] = b0;
-  }
+      for (int v = 0; v < 16; v++) acc[i][j][v] = bias4[j];
 
   auto mfma_fp4_step = [&](int kk, const Fp4Frag& f, const uint32_t (&sa)[4], const uint32_t (&sb)[4]) {
 #pragma unroll
@@ -563,11 +570,16 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     for (int i = 0; i < 4; i++) {
       const v4i x0 = f.p[i][0], x1 = f.p[i][1];
       const int xs[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-      uint32_t hh[8], ll[8];
+      v4i hh, ll;
 #pragma unroll
-      for (int e = 0; e < 8; e++) split_bf16(__int_as_float(xs[e]), hh[e], ll[e]);
-      ahi[i] = pack_v8bf(hh);
-      alo[i] = pack_v8bf(ll);
+      for (int e = 0; e < 4; e++) {
+        uint32_t hp, lp;
+        split_bf16x2(__int_as_float(xs[2 * e]), __int_as_float(xs[2 * e + 1]), hp, lp);
+        hh[e] = (int)hp;
+        ll[e] = (int)lp;
+      }
+      ahi[i] = __builtin_bit_cast(v8bf, hh);
+      alo[i] = __builtin_bit_cast(v8bf, ll);
     }
 #pragma unroll
     for (int i = 0; i < 4; i++)
@@ -739,17 +751,29 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
           *(v2i*)(ow + cc * CS + rr * 2) = w;
         }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // the wave reads back only its own area
+    // Two batches of 16 row segments: all reads of a batch, then its stores
+    // (buffer stores; rows or columns past the edge get an out-of-range offset).
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(out, (uint32_t)M * NO * 2);
     const int src_col = 8 * (t16 & 3) + (t16 >> 2);
 #pragma unroll
-    for (int it = 0; it < 32; it++) {
-      const int cb = 32 * (it & 3), rb = 16 * (it >> 2) + 4 * g16;
-      const FT_LDS uint8_t* p = (const FT_LDS uint8_t*)ow + (cb + src_col) * CS + rb * 2;
-      const v4s lo = lds_read_tr16(p), hi = lds_read_tr16(p + 4 * CS);
-      const int gr = m0 + wm * 128 + rb + (t16 & 3), gc = n0 + wn * 128 + cb + 8 * (t16 >> 2);
-      if (gr < M && gc < NO)
-        *(v4i*)((uint16_t*)out + (size_t)gr * NO + gc) =
-            v4i{(int)(((uint32_t)(uint16_t)lo[1] << 16) | (uint16_t)lo[0]), (int)(((uint32_t)(uint16_t)lo[3] << 16) | (uint16_t)lo[2]),
-                (int)(((uint32_t)(uint16_t)hi[1] << 16) | (uint16_t)hi[0]), (int)(((uint32_t)(uint16_t)hi[3] << 16) | (uint16_t)hi[2])};
+    for (int half = 0; half < 2; half++) {
+      v4i seg[16];
+#pragma unroll
+      for (int k = 0; k < 16; k++) {
+        const int it = 16 * half + k;
+        const int cb = 32 * (it & 3), rb = 16 * (it >> 2) + 4 * g16;
+        const FT_LDS uint8_t* p = (const FT_LDS uint8_t*)ow + (cb + src_col) * CS + rb * 2;
+        const v4s lo = lds_read_tr16(p), hi = lds_read_tr16(p + 4 * CS);
+        seg[k] = __builtin_bit_cast(v4i, make_v8bf(lo, hi));
+      }
+#pragma unroll
+      for (int k = 0; k < 16; k++) {
+        const int it = 16 * half + k;
+        const int cb = 32 * (it & 3), rb = 16 * (it >> 2) + 4 * g16;
+        const int gr = m0 + wm * 128 + rb + (t16 & 3), gc = n0 + wn * 128 + cb + 8 * (t16 >> 2);
+        const uint32_t off = (gr < M && gc < NO) ? ((uint32_t)gr * NO + gc) * 2 : kOobOffset;
+        __builtin_amdgcn_raw_buffer_store_b128(seg[k], ro, off, 0, 0);
+      }
     }
   }
 }
@@ -762,7 +786,7 @@ hipError_t launch_gemm_fp4(bool bwd, const uint8_t* a, const uint8_t* as, const 
   const int tm = (M + GB - 1) / GB, tn = (NO + GB - 1) / GB;
   // buffer ranges are 32-bit: the pipelined kernel takes operands below 2 GiB
   const bool small = (size_t)M * KR / 2 < (1u << 31) && (size_t)N * K / 2 < (1u << 31) &&
-                     (size_t)M * (R > 0 ? R : 1) * 4 < (1u << 31);
+                     (size_t)M * (R > 0 ? R : 1) * 4 < (1u << 31) && (size_t)M * NO * 2 < (1u << 31);
   if (KR % PK == 0 && K % 128 == 0 && small) {
     const unsigned grid = (unsigned)(tm * tn);
     if (!bwd) {

@@ -9,7 +9,8 @@
 // (hi + lo) so that its ~16 leading bits take part.
 //
 // Workgroup = 4 waves over 128 output columns (32 per wave) and one chunk of
-// the token axis; chunks meet in fp32 atomics.  Stages move through an LDS
+// the token axis.  With several chunks each one stores its fp32 partial in a
+// workspace and a reduction kernel sums them in a fixed order.  Stages move through an LDS
 // ring with buffer loads that write LDS directly, one or two stages ahead of
 // the one on the matrix cores.  The two k-halves of an MFMA take the even and
 // odd rows of a 16-row step, which keeps the 32-bit L reads conflict-free.
@@ -46,6 +47,7 @@ struct LoraJob {
   int ncg;              // column groups of LG_WC
   uint32_t v_bytes;     // rows * C * 2  (< 2^31)
   uint32_t l_bytes;     // rows * ld * 4 (< 2^31)
+  size_t part_off;      // offset of this output within a workspace part (floats)
 };
 
 // 16-byte chunk swizzle of a V row (16 chunks): rows 0..7 of a group spread
@@ -55,7 +57,8 @@ __device__ __forceinline__ int lg_swz(int row, int chunk) { return chunk ^ ((row
 // One workgroup's share: output columns [c0, c0 + LG_WC) of `job` over token
 // rows [mbeg, mend).  DB selects the operand roles and the store layout.
 template <int RTJ, bool DB>
-__device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int c0, int mbeg, int mend, int ld, int r) {
+__device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int c0, int mbeg, int mend, int ld, int r,
+                                          float* part, int accumulate) {
   using G = LoraGeom<RTJ>;
   const int nst = (mend - mbeg + LG_BM - 1) / LG_BM;
 
@@ -131,10 +134,15 @@ __device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int 
 #pragma unroll
       for (int t = 0; t < RTJ; t++) {
         const FT_LDS float* lp = (const FT_LDS float*)(sb + l_rd + ks * 16 * G::LROW + t * 128);
-        uint32_t hi[8], lo[8];
+        v4i hi, lo;
 #pragma unroll
-        for (int e = 0; e < 8; e++) split_bf16(lp[2 * e * (G::LROW / 4)], hi[e], lo[e]);
-        const v8bf ah = pack_v8bf(hi), al = pack_v8bf(lo);
+        for (int e = 0; e < 4; e++) {
+          uint32_t hp, lq;
+          split_bf16x2(lp[4 * e * (G::LROW / 4)], lp[(4 * e + 2) * (G::LROW / 4)], hp, lq);
+          hi[e] = (int)hp;
+          lo[e] = (int)lq;
+        }
+        const v8bf ah = __builtin_bit_cast(v8bf, hi), al = __builtin_bit_cast(v8bf, lo);
         if constexpr (DB) {
           acc[t] = mfma_bf16_32x32x16(ah, vf, acc[t]);
           acc[t] = mfma_bf16_32x32x16(al, vf, acc[t]);
@@ -157,15 +165,18 @@ __device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int 
       const int j = DB ? t * 32 + tr : t * 32 + l32;
       const int c = c0 + 32 * wave + (DB ? l32 : tr);
       if (j < r && c < job.C) {
-        float* dst = DB ? job.out + (size_t)j * job.C + c : job.out + (size_t)c * r + j;
-        atomicAdd(dst, acc[t][v]);
+        const size_t idx = DB ? (size_t)j * job.C + c : (size_t)c * r + j;
+        if (part) part[job.part_off + idx] = acc[t][v];
+        else job.out[idx] = accumulate ? job.out[idx] + acc[t][v] : acc[t][v];
       }
     }
 }
 
+// parts: nmch workspace parts of part_len floats, or NULL when one chunk covers
+// the token axis (outputs written directly, added to when accumulate).
 template <int RTJ>
 __global__ __launch_bounds__(256) void k_lora_grads(LoraJob jb0, LoraJob jb1, int M, int ld, int r, int mchunk,
-                                                    int nmch) {
+                                                    int nmch, float* parts, size_t part_len, int accumulate) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[LoraGeom<RTJ>::NS * LoraGeom<RTJ>::SLOT];
   int b = blockIdx.x;
   const int n0 = jb0.ncg * nmch;
@@ -174,51 +185,68 @@ __global__ __launch_bounds__(256) void k_lora_grads(LoraJob jb0, LoraJob jb1, in
   const LoraJob& job = second ? jb1 : jb0;
   const int cg = b % job.ncg, mc = b / job.ncg;
   const int mbeg = mc * mchunk, mend = min(M, mbeg + mchunk);
-  if (job.out_rows_are_j) lora_tile<RTJ, true>(job, lds, cg * LG_WC, mbeg, mend, ld, r);
-  else lora_tile<RTJ, false>(job, lds, cg * LG_WC, mbeg, mend, ld, r);
+  float* part = parts ? parts + (size_t)mc * part_len : nullptr;
+  if (job.out_rows_are_j) lora_tile<RTJ, true>(job, lds, cg * LG_WC, mbeg, mend, ld, r, part, accumulate);
+  else lora_tile<RTJ, false>(job, lds, cg * LG_WC, mbeg, mend, ld, r, part, accumulate);
 }
 
-template <int RTJ>
-static void launch_lg(const LoraJob& jobB, const LoraJob& jobA, int rows, int ld, int r, hipStream_t st) {
-  // one round of workgroups: ring LDS allows two per CU up to RTJ 3, one at RTJ 4
-  const int slots = (2 * LoraGeom<RTJ>::NS * LoraGeom<RTJ>::SLOT <= 160 * 1024 ? 2 : 1) * 256;
-  const int ncg = jobB.ncg + jobA.ncg;
+// Token chunking: enough workgroups for one round (ring LDS allows two per
+// CU up to RTJ 3, one at RTJ 4).
+static void lg_geometry(int rows, int K, int N, int r, int& nmch, int& mchunk) {
+  const int rtj = (r + 31) / 32;
+  const int slot_bytes = LG_VBYTES + LG_BM * rtj * 128, ns = rtj == 1 ? 3 : 2;
+  const int slots = (2 * ns * slot_bytes <= 160 * 1024 ? 2 : 1) * 256;
+  const int ncg = (N + LG_WC - 1) / LG_WC + (K + LG_WC - 1) / LG_WC;
   const int mblocks = (rows + LG_BM - 1) / LG_BM;
-  int nmch = std::max(1, std::min(mblocks, slots / ncg));
-  const int mchunk = ((mblocks + nmch - 1) / nmch) * LG_BM;
+  nmch = std::max(1, std::min(mblocks, slots / ncg));
+  mchunk = ((mblocks + nmch - 1) / nmch) * LG_BM;
   nmch = (rows + mchunk - 1) / mchunk;
-  k_lora_grads<RTJ><<<(unsigned)(ncg * nmch), 256, 0, st>>>(jobB, jobA, rows, ld, r, mchunk, nmch);
+}
+
+// Token windows small enough that every buffer stays below 2 GiB, so the
+// out-of-range offset used for masked lanes is beyond every buffer.
+static size_t lg_window(int M, int K, int N, int ld) {
+  const size_t lim = (size_t)1 << 31;
+  const size_t seg = std::min(lim / ((size_t)std::max(K, N) * 2), lim / ((size_t)ld * 4));
+  return std::min((size_t)M, seg / LG_BM * LG_BM);
+}
+
+size_t lora_grads_workspace(int M, int K, int N, int ld, int r) {
+  if (M == 0) return 0;
+  const size_t seg = lg_window(M, K, N, ld);
+  if (seg == 0) return 0;
+  int nmch, mchunk;
+  lg_geometry((int)seg, K, N, r, nmch, mchunk);   // the first window has the most chunks
+  return nmch > 1 ? (size_t)nmch * r * ((size_t)N + K) * sizeof(float) : 0;
 }
 
 hipError_t launch_lora_grads(const uint16_t* x, int M, int K, const uint16_t* dy, int N, const float* xa,
-                             const float* dyb, int ld, int r, float* dA, float* dB, bool accumulate,
+                             const float* dyb, int ld, int r, float* dA, float* dB, bool accumulate, float* ws,
                              hipStream_t st) {
-  if (!accumulate) {
-    hipError_t e = launch_fill_f32(dA, (size_t)K * r, 0.0f, st);
-    if (e != hipSuccess) return e;
-    e = launch_fill_f32(dB, (size_t)r * N, 0.0f, st);
-    if (e != hipSuccess) return e;
-  }
-  if (M == 0) return hipSuccess;
-  // Token windows small enough that every buffer stays below 2 GiB, so the
-  // out-of-range offset used for masked lanes is beyond every buffer.
-  const size_t lim = (size_t)1 << 31;
-  size_t seg = std::min(lim / ((size_t)std::max(K, N) * 2), lim / ((size_t)ld * 4));
-  seg = std::min((size_t)M, seg / LG_BM * LG_BM);
+  if (M == 0)  // empty sums: zeros (a reduction over no parts), or nothing to add
+    return accumulate ? hipSuccess : launch_reduce_parts(nullptr, 0, (size_t)r * N, dB, (size_t)K * r, dA, false, st);
+  const size_t seg = lg_window(M, K, N, ld);
   if (seg == 0) return hipErrorInvalidValue;
+  const size_t part_len = (size_t)r * ((size_t)N + K);
   for (size_t m0 = 0; m0 < (size_t)M; m0 += seg) {
     const int rows = (int)std::min(seg, (size_t)M - m0);
+    const bool acc = accumulate || m0 > 0;
     const LoraJob jobB{xa + m0 * ld, dy + m0 * N, dB, N, 1, (N + LG_WC - 1) / LG_WC,
-                       (uint32_t)((size_t)rows * N * 2), (uint32_t)((size_t)rows * ld * 4)};
+                       (uint32_t)((size_t)rows * N * 2), (uint32_t)((size_t)rows * ld * 4), 0};
     const LoraJob jobA{dyb + m0 * ld, x + m0 * K, dA, K, 0, (K + LG_WC - 1) / LG_WC,
-                       (uint32_t)((size_t)rows * K * 2), (uint32_t)((size_t)rows * ld * 4)};
+                       (uint32_t)((size_t)rows * K * 2), (uint32_t)((size_t)rows * ld * 4), (size_t)r * N};
+    int nmch, mchunk;
+    lg_geometry(rows, K, N, r, nmch, mchunk);
+    float* parts = nmch > 1 ? ws : nullptr;
+    const unsigned grid = (unsigned)((jobB.ncg + jobA.ncg) * nmch);
     switch ((r + 31) / 32) {
-      case 1: launch_lg<1>(jobB, jobA, rows, ld, r, st); break;
-      case 2: launch_lg<2>(jobB, jobA, rows, ld, r, st); break;
-      case 3: launch_lg<3>(jobB, jobA, rows, ld, r, st); break;
-      default: launch_lg<4>(jobB, jobA, rows, ld, r, st); break;
+      case 1: k_lora_grads<1><<<grid, 256, 0, st>>>(jobB, jobA, rows, ld, r, mchunk, nmch, parts, part_len, acc); break;
+      case 2: k_lora_grads<2><<<grid, 256, 0, st>>>(jobB, jobA, rows, ld, r, mchunk, nmch, parts, part_len, acc); break;
+      case 3: k_lora_grads<3><<<grid, 256, 0, st>>>(jobB, jobA, rows, ld, r, mchunk, nmch, parts, part_len, acc); break;
+      default: k_lora_grads<4><<<grid, 256, 0, st>>>(jobB, jobA, rows, ld, r, mchunk, nmch, parts, part_len, acc); break;
     }
     hipError_t e = hipGetLastError();
+    if (e == hipSuccess && parts) e = launch_reduce_parts(parts, nmch, (size_t)r * N, dB, (size_t)K * r, dA, acc, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

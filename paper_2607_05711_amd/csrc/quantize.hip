@@ -49,7 +49,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
                                                                      int cols, uint8_t* __restrict__ codes,
                                                                      uint8_t* __restrict__ scales,
                                                                      const uint16_t* __restrict__ proj, int R,
-                                                                     float* __restrict__ proj_out, int use_atomics) {
+                                                                     float* __restrict__ proj_out, float* __restrict__ parts) {
   using L = QuantLds<RT, MODE, WAVES, CW>;
   __shared__ __attribute__((aligned(16))) uint16_t lds[L::HALFWORDS];
   constexpr int NST = CW / 64;     // 64-column steps per chunk
@@ -176,6 +176,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
   }
 
   if constexpr (MODE != 0) {
+    // this chunk's partial (several chunks) or the projection itself (one chunk)
+    float* dst = parts ? parts + (size_t)blockIdx.y * rows * R : proj_out;
 #pragma unroll
     for (int t = 0; t < RT; t++) {
       const int j = t * 32 + r32;
@@ -183,11 +185,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
 #pragma unroll
       for (int v = 0; v < 16; v++) {
         const int rr = rw0 + 8 * (v >> 2) + 4 * h + (v & 3);
-        if (rr < rows) {
-          float* dst = proj_out + (size_t)rr * R + j;
-          if (use_atomics) atomicAdd(dst, acc[t][v]);
-          else *dst = acc[t][v];
-        }
+        if (rr < rows) dst[(size_t)rr * R + j] = acc[t][v];
       }
     }
   }
@@ -230,49 +228,50 @@ __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict_
   if (lane == 0) scales[(size_t)tr * nbc + tc] = (uint8_t)code;
 }
 
-// Fill with 16-byte stores (p is 16-byte aligned); the last n % 4 floats singly.
-__global__ void k_fill_f32(float* __restrict__ p, size_t n, float v) {
-  const size_t n4 = n >> 2;
-  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t st = (size_t)gridDim.x * blockDim.x;
-  for (size_t j = i; j < n4; j += st) ((float4*)p)[j] = make_float4(v, v, v, v);
-  if (i < (n & 3)) p[4 * n4 + i] = v;
-}
-
 // ---------------------------------------------------------------- launchers
-template <int RT, int MODE, int WAVES, int CW>
-static hipError_t launch_rows_t(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
-                                const uint16_t* proj, int R, float* proj_out, hipStream_t st) {
-  dim3 grid((rows + 32 * WAVES - 1) / (32 * WAVES), (cols + CW - 1) / CW);
-  const int atomics = MODE != 0 && grid.y > 1;
-  if (atomics) {
-    hipError_t e = launch_fill_f32(proj_out, (size_t)rows * R, 0.0f, st);
-    if (e != hipSuccess) return e;
-  }
-  k_quant_rows<RT, MODE, WAVES, CW><<<grid, 64 * WAVES, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, atomics);
-  return hipGetLastError();
-}
-
 // Geometry per mode, from timing at the FLUX shapes: 8 waves (256 rows) per
 // workgroup amortize the staged projection chunk; the [R, cols] projection
-// takes 768-column chunks (fewer atomic partial sums) while the chunk fits LDS.
+// takes 768-column chunks (fewer partial sums) while the chunk fits LDS.
+static int quant_chunk_cols(int R, int layout) {
+  if (R == 0 || layout == 0) return 384;
+  return (R + 31) / 32 <= 2 ? 768 : 384;
+}
+
+size_t quant_rows_workspace(int rows, int cols, int R, int layout) {
+  if (R == 0) return 0;
+  const int chunks = (cols + quant_chunk_cols(R, layout) - 1) / quant_chunk_cols(R, layout);
+  return chunks > 1 ? (size_t)chunks * rows * R * sizeof(float) : 0;
+}
+
+template <int RT, int MODE, int WAVES, int CW>
+static hipError_t launch_rows_t(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
+                                const uint16_t* proj, int R, float* proj_out, float* ws, hipStream_t st) {
+  dim3 grid((rows + 32 * WAVES - 1) / (32 * WAVES), (cols + CW - 1) / CW);
+  float* parts = MODE != 0 && grid.y > 1 ? ws : nullptr;
+  k_quant_rows<RT, MODE, WAVES, CW><<<grid, 64 * WAVES, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, parts);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !parts) return e;
+  return launch_reduce_parts(parts, (int)grid.y, (size_t)rows * R, proj_out, 0, nullptr, false, st);
+}
+
 hipError_t launch_quant_rows(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
-                             const uint16_t* proj, int R, int layout, float* proj_out, hipStream_t st) {
-  if (!proj || R == 0) return launch_rows_t<1, 0, 4, 384>(src, rows, cols, codes, scales, nullptr, 0, nullptr, st);
+                             const uint16_t* proj, int R, int layout, float* proj_out, float* ws, hipStream_t st) {
+  if (!proj || R == 0)
+    return launch_rows_t<1, 0, 4, 384>(src, rows, cols, codes, scales, nullptr, 0, nullptr, nullptr, st);
   const int rt = (R + 31) / 32;
   if (layout == 0) {
     switch (rt) {
-      case 1: return launch_rows_t<1, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-      case 2: return launch_rows_t<2, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-      case 3: return launch_rows_t<3, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-      default: return launch_rows_t<4, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+      case 1: return launch_rows_t<1, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+      case 2: return launch_rows_t<2, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+      case 3: return launch_rows_t<3, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+      default: return launch_rows_t<4, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
     }
   }
   switch (rt) {
-    case 1: return launch_rows_t<1, 2, 8, 768>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-    case 2: return launch_rows_t<2, 2, 8, 768>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-    case 3: return launch_rows_t<3, 2, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
-    default: return launch_rows_t<4, 2, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, st);
+    case 1: return launch_rows_t<1, 2, 8, 768>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+    case 2: return launch_rows_t<2, 2, 8, 768>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+    case 3: return launch_rows_t<3, 2, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+    default: return launch_rows_t<4, 2, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
   }
 }
 
@@ -280,12 +279,6 @@ hipError_t launch_quant_tiles(const uint16_t* src, int rows, int cols, uint8_t* 
                               hipStream_t st) {
   const int tiles = (rows / 32) * (cols / 32);
   k_quant_tiles<<<(tiles + 3) / 4, 256, 0, st>>>(src, rows, cols, codes, scales);
-  return hipGetLastError();
-}
-
-hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st) {
-  if (n == 0) return hipSuccess;
-  k_fill_f32<<<(unsigned)std::min<size_t>((n / 4 + 255) / 256 + 1, 2048), 256, 0, st>>>(p, n, v);
   return hipGetLastError();
 }
 

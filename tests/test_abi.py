@@ -58,8 +58,9 @@ MISALIGNED = ctypes.c_void_p(0x100008)
 NULL = None
 
 
-def q(src, rows, cols, block_rows, codes, scales, proj=NULL, R=0, layout=0, out=NULL):
-    return _lib.load().ft_quantize_blockwise(src, rows, cols, block_rows, codes, scales, proj, R, layout, out, NULL)
+def q(src, rows, cols, block_rows, codes, scales, proj=NULL, R=0, layout=0, out=NULL, ws=NULL, wsb=0):
+    return _lib.load().ft_quantize_blockwise(src, rows, cols, block_rows, codes, scales, proj, R, layout, out,
+                                             ws, wsb, NULL)
 
 
 def test_quantize_validation():
@@ -76,6 +77,17 @@ def test_quantize_validation():
     assert q(ALIGNED, 64, 64, 32, ALIGNED, ALIGNED, ALIGNED2, 32, 0, ALIGNED2) == _lib.FT_ERR_UNSUPPORTED
     # empty input is a no-op, even with NULL buffers
     assert q(NULL, 0, 64, 1, NULL, NULL) == _lib.FT_OK
+    # a projection over several column chunks needs the workspace the size query reports
+    need = _lib.ft_quantize_workspace_size(4608, 3072, 1, 64, 0)
+    assert need == 8 * 4608 * 64 * 4                       # 384-column chunks of [cols, R] projections
+    assert _lib.ft_quantize_workspace_size(4608, 9216, 1, 64, 1) == 12 * 4608 * 64 * 4   # 768 for [R, cols]
+    assert _lib.ft_quantize_workspace_size(4608, 384, 1, 64, 0) == 0                     # one chunk: none
+    assert _lib.ft_quantize_workspace_size(4608, 3072, 1, 0, 0) == 0                     # no projection: none
+    assert _lib.ft_quantize_workspace_size(4608, 3072, 32, 0, 0) == 0
+    big = (ALIGNED, 4608, 3072, 1, ALIGNED, ALIGNED, ALIGNED2, 64, 0, ALIGNED2)
+    assert q(*big) == _lib.FT_ERR_NULL
+    assert q(*big, ws=ALIGNED2, wsb=need - 16) == _lib.FT_ERR_SHAPE
+    assert q(*big, ws=MISALIGNED, wsb=need) == _lib.FT_ERR_ALIGN
 
 
 def test_linear_validation():
@@ -102,7 +114,8 @@ def test_lora_validation():
     f = _lib.load().ft_lora_grads
     args = lambda **kw: [kw.get("x", ALIGNED), kw.get("M", 8), kw.get("K", 64), kw.get("dy", ALIGNED), kw.get("N", 64),
                          kw.get("xa", ALIGNED2), kw.get("dyb", ALIGNED2), kw.get("ld", 32), kw.get("r", 16),
-                         kw.get("dA", ALIGNED), kw.get("dB", ALIGNED), kw.get("acc", 0), NULL]
+                         kw.get("dA", ALIGNED), kw.get("dB", ALIGNED), kw.get("acc", 0), kw.get("ws", NULL),
+                         kw.get("wsb", 0), NULL]
     assert f(*args(r=0)) == _lib.FT_ERR_UNSUPPORTED
     assert f(*args(r=129, ld=132)) == _lib.FT_ERR_UNSUPPORTED
     assert f(*args(ld=8)) == _lib.FT_ERR_SHAPE
@@ -115,3 +128,11 @@ def test_lora_validation():
     assert f(*args(xa=MISALIGNED)) == _lib.FT_ERR_ALIGN
     assert f(*args(dyb=MISALIGNED)) == _lib.FT_ERR_ALIGN
     assert f(*args(N=(1 << 24) + 32)) == _lib.FT_ERR_UNSUPPORTED
+    # token chunks leave partial sums in the workspace
+    need = _lib.ft_lora_grads_workspace_size(4608, 3072, 9216, 64, 32)
+    assert need > 0 and need % (32 * (3072 + 9216) * 4) == 0
+    assert _lib.ft_lora_grads_workspace_size(64, 3072, 9216, 64, 32) == 0        # one 64-row stage: no chunks
+    big = dict(M=4608, K=3072, N=9216, ld=64, r=32)
+    assert f(*args(**big)) == _lib.FT_ERR_NULL
+    assert f(*args(**big, ws=ALIGNED2, wsb=need - 4)) == _lib.FT_ERR_SHAPE
+    assert f(*args(**big, ws=MISALIGNED, wsb=need)) == _lib.FT_ERR_ALIGN
