@@ -307,18 +307,21 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
 
   const int nst = KR / PK, nlr = R / 16, total = nst + nlr;
 
-  // Bias of this lane's four output columns (forward), loaded first so its
-  // latency overlaps the first stage loads.
-  float bias4[4] = {0.f, 0.f, 0.f, 0.f};
-  if constexpr (!BWD) {
-    if (bias) {
+  // Accumulator tiles are computed transposed (W fragment as MFMA operand A):
+  // lane (r32, h) of tile acc[i][j] holds output row wm*128 + 32i + r32 and,
+  // in element 4q + e, column wn*128 + 32j + 8q + 4h + e.
+  // Bias of this lane's columns (forward): four bf16 per (j, q), loaded first.
+  uint2 bias4[4][4];
 #pragma unroll
-      for (int j = 0; j < 4; j++) {
-        const int gc = n0 + wn * 128 + j * 32 + r32;
-        if (gc < N) bias4[j] = bf16_to_f32(bias[gc]);
+  for (int j = 0; j < 4; j++)
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+      bias4[j][q] = make_uint2(0u, 0u);
+      if constexpr (!BWD) {
+        const int gc = n0 + wn * 128 + j * 32 + 8 * q + 4 * h;
+        if (bias && gc < N) bias4[j][q] = *(const uint2*)(bias + gc);
       }
     }
-  }
 
   // ---------------- per-lane load geometry (constant over stages)
   // Each buffer load takes a per-lane byte offset (constant over stages; rows
@@ -545,23 +548,15 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     }
   };
 
-  // Accumulators start at the bias (forward): every output column's sum then
-  // begins with its bias term, in both output precisions.
   v16f acc[4][4];
-#pragma unroll
-  for (int j = 0; j < 4; j++)
-#pragma unroll
-    for (int i = 0; i < 4; i++)
-#pragma unroll
-      for (int v = 0; v < 16; v++) acc[i][j][v] = bias4[j];
 
   auto mfma_fp4_step = [&](int kk, const Fp4Frag& f, const uint32_t (&sa)[4], const uint32_t (&sb)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; i++)
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        if (kk == 0) acc[i][j] = mfma_fp4_32x32x64<0>(f.a[i], f.b[j], acc[i][j], (int)sa[i], (int)sb[j]);
-        else acc[i][j] = mfma_fp4_32x32x64<1>(f.a[i], f.b[j], acc[i][j], (int)sa[i], (int)sb[j]);
+        if (kk == 0) acc[i][j] = mfma_fp4_32x32x64<0>(f.b[j], f.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
+        else acc[i][j] = mfma_fp4_32x32x64<1>(f.b[j], f.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
       }
   };
   auto mfma_lr_step = [&](const LrFrag& f) {
@@ -585,8 +580,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     for (int i = 0; i < 4; i++)
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        acc[i][j] = mfma_bf16_32x32x16(ahi[i], f.b[j], acc[i][j]);
-        acc[i][j] = mfma_bf16_32x32x16(alo[i], f.b[j], acc[i][j]);
+        acc[i][j] = mfma_bf16_32x32x16(f.b[j], ahi[i], acc[i][j]);
+        acc[i][j] = mfma_bf16_32x32x16(f.b[j], alo[i], acc[i][j]);
       }
   };
 
@@ -597,6 +592,19 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   issue(0);
   issue(1);
   issue(2);
+  // Accumulators start at the bias (forward): every output's sum begins with
+  // its bias term, in both output precisions.
+#pragma unroll
+  for (int i = 0; i < 4; i++)
+#pragma unroll
+    for (int j = 0; j < 4; j++)
+#pragma unroll
+      for (int q = 0; q < 4; q++) {
+        acc[i][j][4 * q + 0] = bf16_to_f32(bias4[j][q].x & 0xFFFFu);
+        acc[i][j][4 * q + 1] = bf16_to_f32(bias4[j][q].x >> 16);
+        acc[i][j][4 * q + 2] = bf16_to_f32(bias4[j][q].y & 0xFFFFu);
+        acc[i][j][4 * q + 3] = bf16_to_f32(bias4[j][q].y >> 16);
+      }
   publish(loads_of(1) + loads_of(2));
   Fp4Frag f0, f1;
   ScaleRaw sr;
@@ -623,7 +631,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
 #pragma unroll
     for (int m = 0; m < 16; m++) {
       const int i = m >> 2, j = m & 3;
-      acc[i][j] = mfma_fp4_32x32x64<0>(f0.a[i], f0.b[j], acc[i][j], (int)sa[i], (int)sb[j]);
+      acc[i][j] = mfma_fp4_32x32x64<0>(f0.b[j], f0.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
       if (m < FRAG_READS) read_one(t, 1, m, f1);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -635,7 +643,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
 #pragma unroll
     for (int m = 0; m < 16; m++) {
       const int i = m >> 2, j = m & 3;
-      acc[i][j] = mfma_fp4_32x32x64<1>(f1.a[i], f1.b[j], acc[i][j], (int)sa[i], (int)sb[j]);
+      acc[i][j] = mfma_fp4_32x32x64<1>(f1.b[j], f1.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
       // reads of stage t+1: fragments in slots 0..FRAG_READS-1, then scales
       if (m < FRAG_READS) read_one(t + 1, 0, m, f0);
       if (m == FRAG_READS - 4 || (BWD && m == 12)) {
@@ -714,65 +722,51 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   }
 
   // ---------------- epilogue: convert, store
+  const int orow0 = m0 + wm * 128, ocol0 = n0 + wn * 128;   // this wave's 128x128 block
   if constexpr (OUT_F32) {
 #pragma unroll
-    for (int j = 0; j < 4; j++) {
-      const int gc = n0 + wn * 128 + j * 32 + r32;
-      if (gc >= NO) continue;
-#pragma unroll
-      for (int i = 0; i < 4; i++)
-#pragma unroll
-        for (int v = 0; v < 16; v++) {
-          const int gr = m0 + wm * 128 + i * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-          if (gr < M) ((float*)out)[(size_t)gr * NO + gc] = acc[i][j][v];
-        }
-    }
-  } else {
-    // Each wave stages its 128x128 sub-tile in LDS column by column (a lane's
-    // four consecutive rows of one column are one 8-byte write, converted in
-    // pairs), then reads it back row-major with the transposing 16-bit read:
-    // source lane s of a 16-lane group reads 4 rows of column
-    // cb + 8(s%4) + s/4 (+4 in the second read), so output lane i holds
-    // columns cb + 8(i/4) .. +7 of row rb + i%4 and stores them as 16 bytes.
-    __syncthreads();  // all waves are done with the ring
-    constexpr int CS = 128 * 2 + 8;   // bytes per staged column
-    uint8_t* ow = lds + wave * (128 * CS);
-#pragma unroll
-    for (int i = 0; i < 4; i++)
+    for (int i = 0; i < 4; i++) {
+      const int gr = orow0 + 32 * i + r32;
 #pragma unroll
       for (int j = 0; j < 4; j++)
 #pragma unroll
         for (int q = 0; q < 4; q++) {
-          const int rr = i * 32 + 8 * q + 4 * h, cc = j * 32 + r32;
+          const int gc = ocol0 + 32 * j + 8 * q + 4 * h;
+          if (gr < M && gc < NO)
+            *(float4*)((float*)out + (size_t)gr * NO + gc) =
+                make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+        }
+    }
+  } else {
+    // Four passes of 32 rows.  The wave stages the pass's rows in LDS as bf16
+    // (each lane writes its four-column runs, converted in pairs), then reads
+    // them back as 16-byte row segments for coalesced buffer stores (rows or
+    // columns past the edge get an out-of-range offset).
+    __syncthreads();  // all waves are done with the ring
+    constexpr int SROW = 128 * 2 + 16;                 // staged row stride (bytes)
+    uint8_t* stg = lds + wave * (32 * SROW);
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(out, (uint32_t)M * NO * 2);
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+#pragma unroll
+      for (int j = 0; j < 4; j++)
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
           const v2f x01 = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]};
           const v2f x23 = {acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          const v2i w = {(int)__builtin_bit_cast(uint32_t, __builtin_convertvector(x01, v2bf)),
-                         (int)__builtin_bit_cast(uint32_t, __builtin_convertvector(x23, v2bf))};
-          *(v2i*)(ow + cc * CS + rr * 2) = w;
+          *(v2i*)(stg + r32 * SROW + (32 * j + 8 * q + 4 * h) * 2) =
+              v2i{(int)__builtin_bit_cast(uint32_t, __builtin_convertvector(x01, v2bf)),
+                  (int)__builtin_bit_cast(uint32_t, __builtin_convertvector(x23, v2bf))};
         }
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // the wave reads back only its own area
-    // Two batches of 16 row segments: all reads of a batch, then its stores
-    // (buffer stores; rows or columns past the edge get an out-of-range offset).
-    const __amdgpu_buffer_rsrc_t ro = make_rsrc(out, (uint32_t)M * NO * 2);
-    const int src_col = 8 * (t16 & 3) + (t16 >> 2);
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // the wave reads back only its own rows
+      v4i seg[8];
 #pragma unroll
-    for (int half = 0; half < 2; half++) {
-      v4i seg[16];
+      for (int it = 0; it < 8; it++) seg[it] = *(const v4i*)(stg + (4 * it + (lane >> 4)) * SROW + (lane & 15) * 16);
 #pragma unroll
-      for (int k = 0; k < 16; k++) {
-        const int it = 16 * half + k;
-        const int cb = 32 * (it & 3), rb = 16 * (it >> 2) + 4 * g16;
-        const FT_LDS uint8_t* p = (const FT_LDS uint8_t*)ow + (cb + src_col) * CS + rb * 2;
-        const v4s lo = lds_read_tr16(p), hi = lds_read_tr16(p + 4 * CS);
-        seg[k] = __builtin_bit_cast(v4i, make_v8bf(lo, hi));
-      }
-#pragma unroll
-      for (int k = 0; k < 16; k++) {
-        const int it = 16 * half + k;
-        const int cb = 32 * (it & 3), rb = 16 * (it >> 2) + 4 * g16;
-        const int gr = m0 + wm * 128 + rb + (t16 & 3), gc = n0 + wn * 128 + cb + 8 * (t16 >> 2);
+      for (int it = 0; it < 8; it++) {
+        const int gr = orow0 + 32 * i + 4 * it + (lane >> 4), gc = ocol0 + 8 * (lane & 15);
         const uint32_t off = (gr < M && gc < NO) ? ((uint32_t)gr * NO + gc) * 2 : kOobOffset;
-        __builtin_amdgcn_raw_buffer_store_b128(seg[k], ro, off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(seg[it], ro, off, 0, 0);
       }
     }
   }
