@@ -144,6 +144,53 @@ ft_status ft_linear_bwd_input(const uint8_t *gq, const uint8_t *gs, int64_t M, i
                               void *dx, ft_dtype dx_dtype, hipStream_t stream);
 
 /*
+ * MLP pair, forward of FC1 fused with FC2's input preparation (Sec. 3.3, MLP
+ * fusion: the GELU and FC2's quantization and down-projection consume FC1's
+ * output tile while it is on chip).  The GEMM is ft_linear_fwd's; then
+ *   z[m,n]   = bf16(y[m,n])                         saved for the backward
+ *   h[m,n]   = bf16(GELU_tanh(z[m,n]))              FC2's input
+ *   hq, hs   = 1x32 MXFP4 codes/scales of h (as ft_quantize_blockwise)
+ *   P2[m,j]  = sum_n h[m,n] D2[n,j]                 FC2's P (fp32)
+ * GELU_tanh(z) = 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))), evaluated in
+ * fp32.
+ *   Arguments up to bias as ft_linear_fwd.  z, h: bf16 [M, N];  hq uint8
+ *   [M, N/2]; hs uint8 [M, N/32].  D2: bf16 [N, R2] = FC2's [L1 | A];
+ *   R2 in {0, 16, 32, 48, 64} (0: no projection, D2 and P2 NULL);  P2 fp32 [M, R2].
+ *   workspace: ft_linear_fwd_gelu_workspace_size(M, N, R2) bytes, 16-byte
+ *   aligned (NULL when 0): per-column-tile partials of P2, summed in a fixed
+ *   order by a second kernel.
+ * Needs K % 128 == 0 (FT_ERR_UNSUPPORTED otherwise).
+ */
+ft_status ft_linear_fwd_gelu(const uint8_t *xq, const uint8_t *xs, int64_t M, int64_t K,
+                             const uint8_t *wq, const uint8_t *ws, int64_t N,
+                             const float *P, int32_t R, const void *U, const void *bias,
+                             void *z, void *h, uint8_t *hq, uint8_t *hs,
+                             const void *D2, int32_t R2, float *P2,
+                             void *workspace, size_t workspace_bytes, hipStream_t stream);
+size_t ft_linear_fwd_gelu_workspace_size(int64_t M, int64_t N, int32_t R2);
+
+/*
+ * MLP pair, backward-input of FC2 fused with FC1's gradient preparation: the
+ * GEMM is ft_linear_bwd_input's (its fp32 result dH is not rounded), then
+ *   dz[m,k]  = bf16(dH[m,k] * GELU_tanh'(z[m,k]))   FC1's incoming gradient
+ *   dzq, dzs = 1x32 MXFP4 codes/scales of dz
+ *   Qp1[m,j] = sum_k dz[m,k] U1[j,k]                 FC1's Qp (fp32)
+ *   Arguments up to D as ft_linear_bwd_input (N = FC2's output width, K = the
+ *   MLP width).  z: bf16 [M, K] from ft_linear_fwd_gelu.  dz bf16 [M, K];  dzq
+ *   uint8 [M, K/2];  dzs uint8 [M, K/32].  U1: bf16 [R1, K] = FC1's [L2 ; B];
+ *   R1 in {0, 16, 32, 48, 64};  Qp1 fp32 [M, R1].
+ *   workspace: ft_linear_bwd_input_dgelu_workspace_size(M, K, R1) bytes.
+ * Needs N % 128 == 0 and K % 128 == 0 (FT_ERR_UNSUPPORTED otherwise).
+ */
+ft_status ft_linear_bwd_input_dgelu(const uint8_t *gq, const uint8_t *gs, int64_t M, int64_t N,
+                                    const uint8_t *wq, const uint8_t *ws, int64_t K,
+                                    const float *Qp, int32_t R, const void *D,
+                                    const void *z, void *dz, uint8_t *dzq, uint8_t *dzs,
+                                    const void *U1, int32_t R1, float *Qp1,
+                                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+size_t ft_linear_bwd_input_dgelu_workspace_size(int64_t M, int64_t K, int32_t R1);
+
+/*
  * Adapter weight gradients (Sec. 3.2):
  *   dA[k,j] = sum_m X[m,k] dyb[m,j]    (dA = X^T (G B^T))
  *   dB[j,n] = sum_m xa[m,j] G[m,n]     (dB = (X A)^T G)

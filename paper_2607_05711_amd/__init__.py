@@ -5,7 +5,8 @@ in include/fourtune.h); `paper_2607_05711_amd._lib` is its ctypes binding.
 Importing this package does not load the library; the binding loads it on
 first use and raises if it has not been built.
 """
-__all__ = ["ft_quantize_blockwise", "ft_linear_fwd", "ft_linear_bwd_input", "ft_lora_grads"]
+__all__ = ["ft_quantize_blockwise", "ft_linear_fwd", "ft_linear_bwd_input", "ft_lora_grads",
+           "ft_linear_fwd_gelu", "ft_linear_bwd_input_dgelu"]
 
 
 def __getattr__(name):

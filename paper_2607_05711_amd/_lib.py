@@ -52,6 +52,16 @@ def load():
         L.ft_lora_grads.argtypes = [_P, _I64, _I64, _P, _I64, _P, _P, _I64, _I32, _P, _P, _I32, _P, _Z, _P]
         L.ft_lora_grads_workspace_size.argtypes = [_I64, _I64, _I64, _I64, _I32]
         L.ft_lora_grads_workspace_size.restype = _Z
+        L.ft_linear_fwd_gelu.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P,
+                                         _P, _P, _P, _P, _P, _I32, _P, _P, _Z, _P]
+        L.ft_linear_fwd_gelu.restype = ctypes.c_int
+        L.ft_linear_fwd_gelu_workspace_size.argtypes = [_I64, _I64, _I32]
+        L.ft_linear_fwd_gelu_workspace_size.restype = _Z
+        L.ft_linear_bwd_input_dgelu.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P,
+                                                _P, _P, _P, _P, _P, _I32, _P, _P, _Z, _P]
+        L.ft_linear_bwd_input_dgelu.restype = ctypes.c_int
+        L.ft_linear_bwd_input_dgelu_workspace_size.argtypes = [_I64, _I64, _I32]
+        L.ft_linear_bwd_input_dgelu_workspace_size.restype = _Z
         for f in ("ft_quantize_blockwise", "ft_linear_fwd", "ft_linear_bwd_input", "ft_lora_grads"):
             getattr(L, f).restype = ctypes.c_int
         L.ft_status_string.argtypes = [ctypes.c_int]
@@ -215,6 +225,119 @@ def ft_linear_bwd_input(gq, gs, wq, ws, K, Qp=None, D=None, out_dtype=torch.bflo
     _check(L.ft_linear_bwd_input(_ptr(gq), _ptr(gs), M, N, _ptr(wq), _ptr(ws), K, _ptr(Qp), R, _ptr(D),
                                  _ptr(dx), FT_F32 if dx.dtype == torch.float32 else FT_BF16, _stream(dev)))
     return dx
+
+
+def _mlp_outputs(M, C, dev, bf_a, bf_b, codes, scales):
+    e = lambda t, shape, dt: torch.empty(shape, dtype=dt, device=dev) if t is None else t
+    bf_a = e(bf_a, (M, C), torch.bfloat16)
+    bf_b = e(bf_b, (M, C), torch.bfloat16)
+    codes = e(codes, (M, C // 2), torch.uint8)
+    scales = e(scales, (M, C // 32), torch.uint8)
+    for t, n, dt, shape in ((bf_a, "z", torch.bfloat16, (M, C)), (bf_b, "output", torch.bfloat16, (M, C)),
+                            (codes, "codes", torch.uint8, (M, C // 2)), (scales, "scales", torch.uint8, (M, C // 32))):
+        _need(t, n, dt, dev)
+        if tuple(t.shape) != shape:
+            raise ValueError("%s must be %s" % (n, shape))
+    return bf_a, bf_b, codes, scales
+
+
+def ft_linear_fwd_gelu(xq, xs, wq, ws, K, P=None, U=None, bias=None, D2=None, z=None, h=None, hq=None, hs=None,
+                       P2=None, workspace=None):
+    """FC1 forward fused with FC2's input preparation (MLP fusion):
+    z = bf16(y), h = bf16(GELU_tanh(z)), (hq, hs) = MXFP4(h), P2 = h D2.
+    Returns (z, h, hq, hs, P2 or None)."""
+    L = load()
+    dev = xq.device
+    _need(xq, "xq", torch.uint8, ndim=2)
+    _need(xs, "xs", torch.uint8, dev)
+    _need(wq, "wq", torch.uint8, dev, ndim=2)
+    _need(ws, "ws", torch.uint8, dev)
+    M, N = xq.shape[0], wq.shape[0]
+    if xq.shape[1] * 2 != K or wq.shape[1] * 2 != K or xs.numel() * 32 != M * K or ws.numel() * 1024 != N * K:
+        raise ValueError("operand shapes do not match K=%d" % K)
+    R = 0
+    if P is not None or U is not None:
+        _need(P, "P", torch.float32, dev, ndim=2)
+        _need(U, "U", torch.bfloat16, dev, ndim=2)
+        R = P.shape[1]
+        if P.shape[0] != M or U.shape != (R, N):
+            raise ValueError("P [M,R] / U [R,N] shapes mismatch")
+    if bias is not None:
+        _need(bias, "bias", torch.bfloat16, dev)
+        if bias.numel() != N:
+            raise ValueError("bias must have N elements")
+    z, h, hq, hs = _mlp_outputs(M, N, dev, z, h, hq, hs)
+    R2 = 0
+    if D2 is not None:
+        _need(D2, "D2", torch.bfloat16, dev, ndim=2)
+        if D2.shape[0] != N:
+            raise ValueError("D2 must be [N, R2]")
+        R2 = D2.shape[1]
+        if P2 is None:
+            P2 = torch.empty((M, R2), dtype=torch.float32, device=dev)
+        _need(P2, "P2", torch.float32, dev)
+        if P2.shape != (M, R2):
+            raise ValueError("P2 must be [M, R2]")
+    else:
+        P2 = None
+    workspace = _workspace(L.ft_linear_fwd_gelu_workspace_size(M, N, R2), dev, workspace)
+    _check(L.ft_linear_fwd_gelu(_ptr(xq), _ptr(xs), M, K, _ptr(wq), _ptr(ws), N, _ptr(P), R, _ptr(U), _ptr(bias),
+                                _ptr(z), _ptr(h), _ptr(hq), _ptr(hs), _ptr(D2), R2, _ptr(P2),
+                                _ptr(workspace), _nbytes(workspace), _stream(dev)))
+    return z, h, hq, hs, P2
+
+
+def ft_linear_bwd_input_dgelu(gq, gs, wq, ws, K, z, Qp=None, D=None, U1=None, dz=None, dzq=None, dzs=None,
+                              Qp1=None, workspace=None):
+    """FC2 backward-input fused with FC1's gradient preparation:
+    dz = bf16(dH * GELU_tanh'(z)) with dH = DQ(gq) DQ(wq) + Qp D^T in fp32,
+    (dzq, dzs) = MXFP4(dz), Qp1 = dz U1^T.  Returns (dz, dzq, dzs, Qp1 or None)."""
+    L = load()
+    dev = gq.device
+    _need(gq, "gq", torch.uint8, ndim=2)
+    _need(gs, "gs", torch.uint8, dev)
+    _need(wq, "wq", torch.uint8, dev, ndim=2)
+    _need(ws, "ws", torch.uint8, dev)
+    M, N = gq.shape[0], wq.shape[0]
+    if gq.shape[1] * 2 != N or wq.shape[1] * 2 != K or gs.numel() * 32 != M * N or ws.numel() * 1024 != N * K:
+        raise ValueError("operand shapes do not match N=%d K=%d" % (N, K))
+    _need(z, "z", torch.bfloat16, dev)
+    if tuple(z.shape) != (M, K):
+        raise ValueError("z must be [M, K]")
+    R = 0
+    if Qp is not None or D is not None:
+        _need(Qp, "Qp", torch.float32, dev, ndim=2)
+        _need(D, "D", torch.bfloat16, dev, ndim=2)
+        R = Qp.shape[1]
+        if Qp.shape[0] != M or D.shape != (K, R):
+            raise ValueError("Qp [M,R] / D [K,R] shapes mismatch")
+    _, dz, dzq, dzs = _mlp_outputs(M, K, dev, z, dz, dzq, dzs)
+    R1 = 0
+    if U1 is not None:
+        _need(U1, "U1", torch.bfloat16, dev, ndim=2)
+        if U1.shape[1] != K:
+            raise ValueError("U1 must be [R1, K]")
+        R1 = U1.shape[0]
+        if Qp1 is None:
+            Qp1 = torch.empty((M, R1), dtype=torch.float32, device=dev)
+        _need(Qp1, "Qp1", torch.float32, dev)
+        if Qp1.shape != (M, R1):
+            raise ValueError("Qp1 must be [M, R1]")
+    else:
+        Qp1 = None
+    workspace = _workspace(L.ft_linear_bwd_input_dgelu_workspace_size(M, K, R1), dev, workspace)
+    _check(L.ft_linear_bwd_input_dgelu(_ptr(gq), _ptr(gs), M, N, _ptr(wq), _ptr(ws), K, _ptr(Qp), R, _ptr(D),
+                                       _ptr(z), _ptr(dz), _ptr(dzq), _ptr(dzs), _ptr(U1), R1, _ptr(Qp1),
+                                       _ptr(workspace), _nbytes(workspace), _stream(dev)))
+    return dz, dzq, dzs, Qp1
+
+
+def ft_linear_fwd_gelu_workspace_size(M, N, R2):
+    return int(load().ft_linear_fwd_gelu_workspace_size(M, N, R2))
+
+
+def ft_linear_bwd_input_dgelu_workspace_size(M, K, R1):
+    return int(load().ft_linear_bwd_input_dgelu_workspace_size(M, K, R1))
 
 
 def ft_lora_grads_workspace_size(M, K, N, ld, r):

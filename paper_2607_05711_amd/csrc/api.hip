@@ -146,6 +146,70 @@ ft_status ft_linear_bwd_input(const uint8_t* gq, const uint8_t* gs, int64_t M, i
                     "linear bwd input");
 }
 
+static size_t mlp_workspace(int64_t M, int64_t NO, int32_t R2) {
+  if (M <= 0 || NO <= 0 || R2 <= 0 || M > kMaxDim || NO > kMaxDim) return 0;
+  const int tiles = ft::gemm_fp4_col_tiles((int)NO);
+  return tiles > 1 ? (size_t)tiles * M * R2 * sizeof(float) : 0;
+}
+
+size_t ft_linear_fwd_gelu_workspace_size(int64_t M, int64_t N, int32_t R2) { return mlp_workspace(M, N, R2); }
+
+ft_status ft_linear_fwd_gelu(const uint8_t* xq, const uint8_t* xs, int64_t M, int64_t K, const uint8_t* wq,
+                             const uint8_t* ws, int64_t N, const float* P, int32_t R, const void* U, const void* bias,
+                             void* z, void* h, uint8_t* hq, uint8_t* hs, const void* D2, int32_t R2, float* P2,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  FT_TRY(check_dim("M", M, 1));
+  FT_TRY(check_dim("K", K, 32));
+  FT_TRY(check_dim("N", N, 32));
+  if (M == 0 || N == 0) return FT_OK;
+  if (K == 0) return fail(FT_ERR_SHAPE, "K == 0");
+  if (!xq || !xs || !wq || !ws || !z || !h || !hq || !hs) return fail(FT_ERR_NULL, "xq, xs, wq, ws, z, h, hq, hs are required");
+  if (!aligned16(xq) || !aligned16(wq) || !aligned16(z) || !aligned16(h) || !aligned16(hq) || (bias && !aligned16(bias)))
+    return fail(FT_ERR_ALIGN, "xq, wq, z, h, hq, bias must be 16-byte aligned");
+  FT_TRY(check_rank(R, P, U, "P", "U"));
+  if (R2 != 0 && (R2 < 16 || R2 > 64 || R2 % 16 != 0)) return fail(FT_ERR_UNSUPPORTED, "R2 = %d: need 0 or 16..64, R2 %% 16 == 0", R2);
+  FT_TRY(check_rank(R2, D2, P2, "D2", "P2"));
+  if (!ft::gemm_fp4_fused_supported(false, (int)M, (int)N, (int)K, R, R2))
+    return fail(FT_ERR_UNSUPPORTED, "fused GELU epilogue needs K %% 128 == 0 and operands below 2 GiB");
+  FT_TRY(check_workspace(workspace, workspace_bytes, mlp_workspace(M, N, R2)));
+  const bool parts = mlp_workspace(M, N, R2) > 0;
+  ft::GemmEpilogue ep{(uint16_t*)z, nullptr, (uint16_t*)h, hq, hs, (const uint16_t*)D2, R2, parts ? (float*)workspace : P2};
+  return hip_status(ft::launch_gemm_fp4_fused(false, xq, xs, wq, ws, (int)M, (int)N, (int)K, P, R, (const uint16_t*)U,
+                                              (const uint16_t*)bias, ep, P2, stream),
+                    "linear fwd gelu");
+}
+
+size_t ft_linear_bwd_input_dgelu_workspace_size(int64_t M, int64_t K, int32_t R1) { return mlp_workspace(M, K, R1); }
+
+ft_status ft_linear_bwd_input_dgelu(const uint8_t* gq, const uint8_t* gs, int64_t M, int64_t N, const uint8_t* wq,
+                                    const uint8_t* ws, int64_t K, const float* Qp, int32_t R, const void* D,
+                                    const void* z, void* dz, uint8_t* dzq, uint8_t* dzs, const void* U1, int32_t R1,
+                                    float* Qp1, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  FT_TRY(check_dim("M", M, 1));
+  FT_TRY(check_dim("N", N, 32));
+  FT_TRY(check_dim("K", K, 32));
+  if (M == 0 || K == 0) return FT_OK;
+  if (N == 0) return fail(FT_ERR_SHAPE, "N == 0");
+  if (!gq || !gs || !wq || !ws || !z || !dz || !dzq || !dzs)
+    return fail(FT_ERR_NULL, "gq, gs, wq, ws, z, dz, dzq, dzs are required");
+  if (!aligned16(gq) || !aligned16(wq) || !aligned16(z) || !aligned16(dz) || !aligned16(dzq))
+    return fail(FT_ERR_ALIGN, "gq, wq, z, dz, dzq must be 16-byte aligned");
+  FT_TRY(check_rank(R, Qp, D, "Qp", "D"));
+  if (R1 != 0 && (R1 < 16 || R1 > 64 || R1 % 16 != 0)) return fail(FT_ERR_UNSUPPORTED, "R1 = %d: need 0 or 16..64, R1 %% 16 == 0", R1);
+  FT_TRY(check_rank(R1, U1, Qp1, "U1", "Qp1"));
+  if (!ft::gemm_fp4_fused_supported(true, (int)M, (int)N, (int)K, R, R1))
+    return fail(FT_ERR_UNSUPPORTED, "fused dGELU epilogue needs N and K multiples of 128 and operands below 2 GiB");
+  FT_TRY(check_workspace(workspace, workspace_bytes, mlp_workspace(M, K, R1)));
+  const bool parts = mlp_workspace(M, K, R1) > 0;
+  ft::GemmEpilogue ep{nullptr, (const uint16_t*)z, (uint16_t*)dz, dzq, dzs, (const uint16_t*)U1, R1,
+                      parts ? (float*)workspace : Qp1};
+  return hip_status(ft::launch_gemm_fp4_fused(true, gq, gs, wq, ws, (int)M, (int)N, (int)K, Qp, R, (const uint16_t*)D,
+                                              nullptr, ep, Qp1, stream),
+                    "linear bwd input dgelu");
+}
+
 size_t ft_lora_grads_workspace_size(int64_t M, int64_t K, int64_t N, int64_t ld, int32_t r) {
   if (M <= 0 || K <= 0 || N <= 0 || r < 1 || r > 128 || ld < r || M > kMaxDim || K > (1 << 24) || N > (1 << 24) ||
       ld > 4096)

@@ -69,6 +69,49 @@ __device__ __forceinline__ float e8m0_to_f32(uint32_t code) {
   return __uint_as_float(code ? (code << 23) : 0x00400000u);
 }
 
+// tanh-approximated GELU, 0.5 z (1 + tanh(u)) with u = c0 (z + c1 z^3), and
+// its derivative, in fp32.  With e = exp(-2|u|) (hardware exp2):
+//   1 + tanh(u) = 2 / (1 + e) for u >= 0, 2e / (1 + e) for u < 0,
+//   1 - tanh(u)^2 = 4e / (1 + e)^2,
+// which avoids the cancellation of 1 + tanh(u) for very negative z.
+constexpr float kGeluC0 = 0.7978845608028654f;   // sqrt(2 / pi)
+constexpr float kGeluC1 = 0.044715f;
+struct GeluParts { float one_plus_t, one_minus_t2; };
+__device__ __forceinline__ GeluParts gelu_parts(float z) {
+  const float u = kGeluC0 * (z + kGeluC1 * z * z * z);
+  const float e = __builtin_amdgcn_exp2f(-2.8853900817779268f * fabsf(u));   // exp(-2|u|)
+  const float r = 1.0f / (1.0f + e);
+  return {(u >= 0.0f ? 2.0f : 2.0f * e) * r, 4.0f * e * r * r};
+}
+__device__ __forceinline__ float gelu_tanh(float z) { return 0.5f * z * gelu_parts(z).one_plus_t; }
+__device__ __forceinline__ float gelu_tanh_grad(float z) {
+  const GeluParts g = gelu_parts(z);
+  return 0.5f * g.one_plus_t + 0.5f * z * g.one_minus_t2 * kGeluC0 * (1.0f + 3.0f * kGeluC1 * z * z);
+}
+
+// Quantize 8 consecutive bf16 (packed in w) of a 32-element block held by a
+// lane quad: the block absmax is reduced across the quad with DPP.  Returns
+// the 8 E2M1 codes (element 0 in the low nibble) and the block's E8M0 code.
+__device__ __forceinline__ uint32_t quad_quantize8(const uint32_t (&w)[4], uint32_t& scale_code) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int e = 0; e < 4; e++) {
+    const uint32_t a = w[e] & 0x7FFF7FFFu;
+    m = max(m, max(a & 0xFFFFu, a >> 16));
+  }
+  m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0xB1, 0xF, 0xF, true));  // quad_perm [1,0,3,2]
+  m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0x4E, 0xF, 0xF, true));  // quad_perm [2,3,0,1]
+  scale_code = e8m0_from_amax_bits(m);
+  const float s = e8m0_to_f32(scale_code);
+  uint32_t o = 0;
+  o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[0]), s, 0);
+  o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[1]), s, 1);
+  o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[2]), s, 2);
+  o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[3]), s, 3);
+  return o;
+}
+
+
 // Quantize 32 bf16 values (16 dwords, element 2i in the low half of dword i)
 // to 16 bytes of packed E2M1 codes; returns the E8M0 code.  The conversion
 // instruction divides by the scale, rounds to nearest even and saturates,

@@ -26,6 +26,26 @@ hipError_t launch_gemm_fp4(bool bwd, const uint8_t* a, const uint8_t* as, const 
                            int M, int N, int K, const float* P, int R, const uint16_t* lr,
                            const uint16_t* bias, void* out, bool out_f32, hipStream_t st);
 
+// Epilogues of the MLP pair (the output NO columns feed the next linear).
+enum { EPI_PLAIN = 0, EPI_GELU = 1, EPI_DGELU = 2 };
+struct GemmEpilogue {
+  uint16_t* z_out;        // EPI_GELU: z = bf16(acc) [M, NO]
+  const uint16_t* z_in;   // EPI_DGELU: z saved by the forward [M, NO]
+  uint16_t* y;            // EPI_GELU: h = bf16(GELU(z));  EPI_DGELU: dz = bf16(acc GELU'(z))  [M, NO]
+  uint8_t* q;             // E2M1 codes of y [M, NO/2]
+  uint8_t* s;             // E8M0 scales of y [M, NO/32]
+  const uint16_t* proj;   // EPI_GELU: D2 [NO, R2];  EPI_DGELU: U1 [R2, NO];  unused when R2 == 0
+  int R2;                 // 0, 16, 32, 48 or 64
+  float* parts;           // fp32 partials [tiles over NO][M][R2], or the projection when one tile spans NO
+};
+// Whether the fused epilogues support this shape (the pipelined kernel runs it).
+bool gemm_fp4_fused_supported(bool bwd, int M, int N, int K, int R, int R2);
+// Number of output column tiles (partials of the fused projection).
+int gemm_fp4_col_tiles(int NO);
+hipError_t launch_gemm_fp4_fused(bool bwd, const uint8_t* a, const uint8_t* as, const uint8_t* wq, const uint8_t* ws,
+                                 int M, int N, int K, const float* P, int R, const uint16_t* lr, const uint16_t* bias,
+                                 const GemmEpilogue& ep, float* proj_out, hipStream_t st);
+
 // Adapter gradients; token chunks leave partials in ws (lora_grads_workspace bytes).
 size_t lora_grads_workspace(int M, int K, int N, int ld, int r);
 hipError_t launch_lora_grads(const uint16_t* x, int M, int K, const uint16_t* dy, int N, const float* xa,

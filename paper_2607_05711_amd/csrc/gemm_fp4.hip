@@ -276,13 +276,13 @@ __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, i
   nt = w / gm;
 }
 
-template <bool BWD, bool OUT_F32>
+template <bool BWD, bool OUT_F32, int EPI>
 __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restrict__ A, const uint8_t* __restrict__ As,
                                                           const uint8_t* __restrict__ Wq, const uint8_t* __restrict__ Ws,
                                                           int M, int N, int K, const float* __restrict__ P, int R,
                                                           const uint16_t* __restrict__ LR,
                                                           const uint16_t* __restrict__ bias, void* __restrict__ out,
-                                                          int tiles_m, int tiles_n) {
+                                                          int tiles_m, int tiles_n, GemmEpilogue ep) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[NSLOT * SLOT];
 
   const int NO = BWD ? K : N;
@@ -737,7 +737,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
                 make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
         }
     }
-  } else {
+  } else if constexpr (EPI == EPI_PLAIN) {
     // Four passes of 32 rows.  The wave stages the pass's rows in LDS as bf16
     // (each lane writes its four-column runs, converted in pairs), then reads
     // them back as 16-byte row segments for coalesced buffer stores (rows or
@@ -769,6 +769,155 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         __builtin_amdgcn_raw_buffer_store_b128(seg[it], ro, off, 0, 0);
       }
     }
+  } else {
+    // ---- MLP epilogues (Sec. 3.3, MLP fusion): the output feeds the next
+    // linear directly.
+    //   EPI_GELU  (FC1 forward):  z = bf16(acc) (saved), h = bf16(GELU(z)),
+    //                             h quantized in 1x32 blocks, FC2's down-
+    //                             projection partial h . D2 over this tile.
+    //   EPI_DGELU (FC2 backward-input): dz = bf16(acc * GELU'(z)) with the
+    //                             fp32 acc (dH) unrounded, dz quantized, FC1's
+    //                             partial dz . U1^T over this tile.
+    // Four passes of 32 rows per wave; in each the wave stages its rows in LDS
+    // (bf16 z, or fp32 dH), reads them back as 8-column row segments (a lane
+    // quad holds one 32-column block), writes the outputs and the block codes,
+    // puts the bf16 result back in place, and multiplies its 32x128 rows with
+    // the staged projection slice.  The two waves sharing rows add their
+    // partials through LDS; one stores them.
+    constexpr bool G = EPI == EPI_GELU;
+    constexpr int SROW = G ? 128 * 2 + 16 : 128 * 4 + 16;   // staged row stride (bytes)
+    constexpr int STG = 32 * SROW;
+    constexpr int PS1 = 64 + 16;                            // EPI_GELU slice [256 n][R2 <= 64]: halfwords per row
+    constexpr int PS2 = 256 + 8;                            // EPI_DGELU slice [R2 <= 64][256 k]: halfwords per row
+    constexpr int PSLICE = G ? 256 * PS1 * 2 : 64 * PS2 * 2;
+    uint8_t* stg = lds + wave * STG;
+    uint16_t* ps = (uint16_t*)(lds + 4 * STG);
+    float* comb = (float*)(lds + 4 * STG + PSLICE);          // [2 buffers][2 pairs][32 rows][64]
+    const int R2 = ep.R2;
+    const int tn = nt;
+    __syncthreads();  // all waves are done with the ring
+    if (R2 > 0) {
+      // stage the projection slice: rows n0..n0+255 of D2 [NO, R2], or
+      // columns n0..n0+255 of U1 [R2, NO]; zeros outside
+#pragma unroll
+      for (int u = 0; u < 8; u++) {
+        const int sl = tid + 256 * u;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if constexpr (G) {
+          const int rr = sl >> 3, cc = (sl & 7) * 8;
+          if (n0 + rr < NO && cc < R2) v = *(const uint4*)(ep.proj + (size_t)(n0 + rr) * R2 + cc);
+          *(uint4*)(ps + rr * PS1 + cc) = v;
+        } else {
+          const int rr = sl >> 5, cc = (sl & 31) * 8;
+          if (rr < R2 && n0 + cc < NO) v = *(const uint4*)(ep.proj + (size_t)rr * NO + n0 + cc);
+          *(uint4*)(ps + rr * PS2 + cc) = v;
+        }
+      }
+    }
+    __syncthreads();
+    const __amdgpu_buffer_rsrc_t r_y = make_rsrc(ep.y, (uint32_t)M * NO * 2);
+    const __amdgpu_buffer_rsrc_t r_z = make_rsrc(G ? (const void*)ep.z_out : (const void*)ep.z_in, (uint32_t)M * NO * 2);
+    const __amdgpu_buffer_rsrc_t r_q = make_rsrc(ep.q, (uint32_t)M * (NO / 2));
+    const int g16 = lane >> 4, t16 = lane & 15, jj = t16 >> 2, qq = t16 & 3;
+    const int rt2 = (R2 + 31) >> 5;
+#pragma unroll   // acc[i] must be indexed by constants
+    for (int i = 0; i < 4; i++) {
+      // 1) stage this pass's 32 rows
+#pragma unroll
+      for (int j = 0; j < 4; j++)
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+          const int col = 32 * j + 8 * q + 4 * h;
+          if constexpr (G) {
+            const v2f x01 = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]};
+            const v2f x23 = {acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            *(v2i*)(stg + r32 * SROW + col * 2) =
+                v2i{(int)__builtin_bit_cast(uint32_t, __builtin_convertvector(x01, v2bf)),
+                    (int)__builtin_bit_cast(uint32_t, __builtin_convertvector(x23, v2bf))};
+          } else {
+            *(float4*)(stg + r32 * SROW + col * 4) =
+                make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+          }
+        }
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      // 2) row segments: outputs, block codes, bf16 result back in place
+#pragma unroll 2
+      for (int it = 0; it < 8; it++) {
+        const int rl = 4 * it + g16, seg = t16;
+        const int gr = orow0 + 32 * i + rl, gc = ocol0 + 8 * seg;
+        const bool inb = gr < M && gc < NO;
+        const uint32_t off2 = inb ? ((uint32_t)gr * NO + gc) * 2 : kOobOffset;
+        uint8_t* srow = stg + rl * SROW;
+        uint32_t w[4];
+        if constexpr (G) {
+          const v4i zb = *(const v4i*)(srow + seg * 16);
+          __builtin_amdgcn_raw_buffer_store_b128(zb, r_z, off2, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 4; e++) {
+            const v2f hv = {gelu_tanh(bf16_to_f32((uint32_t)zb[e] & 0xFFFFu)), gelu_tanh(bf16_to_f32((uint32_t)zb[e] >> 16))};
+            w[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(hv, v2bf));
+          }
+        } else {
+          const float4 d0 = *(const float4*)(srow + seg * 32), d1 = *(const float4*)(srow + seg * 32 + 16);
+          const v4i zb = __builtin_amdgcn_raw_buffer_load_b128(r_z, off2, 0, 0);
+          const float dh[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+#pragma unroll
+          for (int e = 0; e < 4; e++) {
+            const v2f dv = {dh[2 * e] * gelu_tanh_grad(bf16_to_f32((uint32_t)zb[e] & 0xFFFFu)),
+                            dh[2 * e + 1] * gelu_tanh_grad(bf16_to_f32((uint32_t)zb[e] >> 16))};
+            w[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(dv, v2bf));
+          }
+        }
+        const v4i wv = {(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+        __builtin_amdgcn_raw_buffer_store_b128(wv, r_y, off2, 0, 0);
+        *(v4i*)(srow + seg * 16) = wv;   // bf16 result in place (for the projection)
+        uint32_t sc;
+        const uint32_t codes = quad_quantize8(w, sc);
+        __builtin_amdgcn_raw_buffer_store_b32((int)codes, r_q, inb ? (uint32_t)gr * (NO / 2) + gc / 2 : kOobOffset, 0, 0);
+        if (inb && (lane & 3) == 0) ep.s[(size_t)gr * (NO / 32) + gc / 32] = (uint8_t)sc;
+      }
+      if (R2 == 0) continue;
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      // 3) projection of the pass's 32 rows over this wave's 128 columns
+      v16f pacc[2] = {v16f{}, v16f{}};
+#pragma unroll
+      for (int ks = 0; ks < 8; ks++) {
+        const v8bf a = __builtin_bit_cast(v8bf, *(const v4i*)(stg + r32 * SROW + (16 * ks + 8 * h) * 2));
+        const int kloc = wn * 128 + 16 * ks + 8 * h;      // column within the workgroup's 256
+#pragma unroll
+        for (int t = 0; t < 2; t++) {
+          if (t >= rt2) break;
+          v8bf b;
+          if constexpr (G) {
+            const uint16_t* base = ps + (kloc + jj) * PS1 + 32 * t + 16 * (g16 & 1) + 4 * qq;
+            b = make_v8bf(lds_read_tr16((const FT_LDS void*)base), lds_read_tr16((const FT_LDS void*)(base + 4 * PS1)));
+          } else {
+            b = __builtin_bit_cast(v8bf, *(const v4i*)(ps + (32 * t + r32) * PS2 + kloc));
+          }
+          pacc[t] = mfma_bf16_32x32x16(a, b, pacc[t]);
+        }
+      }
+      // 4) the two waves with these rows (wn = 0, 1) add their partials
+      float* cb = comb + ((i & 1) * 2 + wm) * (32 * 64);
+      if (wn == 1) {
+#pragma unroll
+        for (int t = 0; t < 2; t++)
+#pragma unroll
+          for (int v = 0; v < 16; v++) cb[(8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * t + r32] = pacc[t][v];
+      }
+      __syncthreads();
+      if (wn == 0) {
+        float* dst = tiles_n > 1 ? ep.parts + (size_t)tn * M * R2 : ep.parts;
+#pragma unroll
+        for (int t = 0; t < 2; t++)
+#pragma unroll
+          for (int v = 0; v < 16; v++) {
+            const int rr = 8 * (v >> 2) + 4 * h + (v & 3), j = 32 * t + r32;
+            const int gr = orow0 + 32 * i + rr;
+            if (j < R2 && gr < M) dst[(size_t)gr * R2 + j] = pacc[t][v] + cb[rr * 64 + j];
+          }
+      }
+    }
   }
 }
 
@@ -783,12 +932,13 @@ hipError_t launch_gemm_fp4(bool bwd, const uint8_t* a, const uint8_t* as, const 
                      (size_t)M * (R > 0 ? R : 1) * 4 < (1u << 31) && (size_t)M * NO * 2 < (1u << 31);
   if (KR % PK == 0 && K % 128 == 0 && small) {
     const unsigned grid = (unsigned)(tm * tn);
+    const GemmEpilogue none{};
     if (!bwd) {
-      if (out_f32) k_gemm_fp4_pipe<false, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out, tm, tn);
-      else k_gemm_fp4_pipe<false, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out, tm, tn);
+      if (out_f32) k_gemm_fp4_pipe<false, true, EPI_PLAIN><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out, tm, tn, none);
+      else k_gemm_fp4_pipe<false, false, EPI_PLAIN><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out, tm, tn, none);
     } else {
-      if (out_f32) k_gemm_fp4_pipe<true, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out, tm, tn);
-      else k_gemm_fp4_pipe<true, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out, tm, tn);
+      if (out_f32) k_gemm_fp4_pipe<true, true, EPI_PLAIN><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out, tm, tn, none);
+      else k_gemm_fp4_pipe<true, false, EPI_PLAIN><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out, tm, tn, none);
     }
     return hipGetLastError();
   }
@@ -801,6 +951,32 @@ hipError_t launch_gemm_fp4(bool bwd, const uint8_t* a, const uint8_t* as, const 
     else k_gemm_fp4_generic<true, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out);
   }
   return hipGetLastError();
+}
+
+static bool pipe_ok(bool bwd, int M, int N, int K, int R) {
+  const int NO = bwd ? K : N, KR = bwd ? N : K;
+  return KR % PK == 0 && K % 128 == 0 && (size_t)M * KR / 2 < (1u << 31) && (size_t)N * K / 2 < (1u << 31) &&
+         (size_t)M * (R > 0 ? R : 1) * 4 < (1u << 31) && (size_t)M * NO * 2 < (1u << 31);
+}
+
+bool gemm_fp4_fused_supported(bool bwd, int M, int N, int K, int R, int R2) {
+  return pipe_ok(bwd, M, N, K, R) && R2 >= 0 && R2 <= 64 && R2 % 16 == 0 &&
+         (size_t)M * (R2 > 0 ? R2 : 1) * 4 < (1u << 31);
+}
+
+int gemm_fp4_col_tiles(int NO) { return (NO + GB - 1) / GB; }
+
+hipError_t launch_gemm_fp4_fused(bool bwd, const uint8_t* a, const uint8_t* as, const uint8_t* wq, const uint8_t* ws,
+                                 int M, int N, int K, const float* P, int R, const uint16_t* lr, const uint16_t* bias,
+                                 const GemmEpilogue& ep, float* proj_out, hipStream_t st) {
+  const int NO = bwd ? K : N;
+  const int tm = (M + GB - 1) / GB, tn = (NO + GB - 1) / GB;
+  const unsigned grid = (unsigned)(tm * tn);
+  if (!bwd) k_gemm_fp4_pipe<false, false, EPI_GELU><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, nullptr, tm, tn, ep);
+  else k_gemm_fp4_pipe<true, false, EPI_DGELU><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, nullptr, tm, tn, ep);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || ep.R2 == 0 || tn == 1) return e;
+  return launch_reduce_parts(ep.parts, tn, (size_t)M * ep.R2, proj_out, 0, nullptr, false, st);
 }
 
 }  // namespace ft

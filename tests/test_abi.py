@@ -33,7 +33,8 @@ def declared_functions():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("ft_quantize_blockwise", "ft_linear_fwd", "ft_linear_bwd_input", "ft_lora_grads",
-              "ft_status_string", "ft_last_error"):
+              "ft_linear_fwd_gelu", "ft_linear_bwd_input_dgelu", "ft_quantize_workspace_size",
+              "ft_lora_grads_workspace_size", "ft_status_string", "ft_last_error"):
         assert n in names
 
 
@@ -136,3 +137,37 @@ def test_lora_validation():
     assert f(*args(**big)) == _lib.FT_ERR_NULL
     assert f(*args(**big, ws=ALIGNED2, wsb=need - 4)) == _lib.FT_ERR_SHAPE
     assert f(*args(**big, ws=MISALIGNED, wsb=need)) == _lib.FT_ERR_ALIGN
+
+
+def test_mlp_fused_validation():
+    L = _lib.load()
+    f = L.ft_linear_fwd_gelu
+    # xq, xs, M, K, wq, ws, N, P, R, U, bias, z, h, hq, hs, D2, R2, P2, ws, wsb, stream
+    base = dict(xq=ALIGNED, xs=ALIGNED, M=8, K=256, wq=ALIGNED, ws=ALIGNED, N=256, P=NULL, R=0, U=NULL, bias=NULL,
+                z=ALIGNED, h=ALIGNED, hq=ALIGNED, hs=ALIGNED, D2=NULL, R2=0, P2=NULL, wsp=NULL, wsb=0)
+    order = ["xq", "xs", "M", "K", "wq", "ws", "N", "P", "R", "U", "bias", "z", "h", "hq", "hs", "D2", "R2", "P2",
+             "wsp", "wsb"]
+    call = lambda **kw: f(*[{**base, **kw}[k] for k in order], NULL)
+    assert call(K=160) == _lib.FT_ERR_UNSUPPORTED                     # K % 128 != 0: no fused kernel
+    assert call(R2=8, D2=ALIGNED2, P2=ALIGNED2) == _lib.FT_ERR_UNSUPPORTED
+    assert call(R2=80, D2=ALIGNED2, P2=ALIGNED2) == _lib.FT_ERR_UNSUPPORTED
+    assert call(R2=32, D2=ALIGNED2) == _lib.FT_ERR_NULL
+    assert call(h=NULL) == _lib.FT_ERR_NULL
+    assert call(z=MISALIGNED) == _lib.FT_ERR_ALIGN
+    need = _lib.ft_linear_fwd_gelu_workspace_size(4608, 12288, 64)
+    assert need == 48 * 4608 * 64 * 4                                  # one partial per 256-column tile
+    assert _lib.ft_linear_fwd_gelu_workspace_size(4608, 256, 64) == 0  # one tile: written directly
+    assert _lib.ft_linear_fwd_gelu_workspace_size(4608, 12288, 0) == 0
+    assert call(M=4608, N=12288, R2=64, D2=ALIGNED2, P2=ALIGNED2) == _lib.FT_ERR_NULL
+    g = L.ft_linear_bwd_input_dgelu
+    base_b = dict(gq=ALIGNED, gs=ALIGNED, M=8, N=256, wq=ALIGNED, ws=ALIGNED, K=256, Qp=NULL, R=0, D=NULL,
+                  z=ALIGNED, dz=ALIGNED, dzq=ALIGNED, dzs=ALIGNED, U1=NULL, R1=0, Qp1=NULL, wsp=NULL, wsb=0)
+    order_b = ["gq", "gs", "M", "N", "wq", "ws", "K", "Qp", "R", "D", "z", "dz", "dzq", "dzs", "U1", "R1", "Qp1",
+               "wsp", "wsb"]
+    call_b = lambda **kw: g(*[{**base_b, **kw}[k] for k in order_b], NULL)
+    assert call_b(N=160) == _lib.FT_ERR_UNSUPPORTED                   # reduction not a multiple of 128
+    assert call_b(K=224) == _lib.FT_ERR_UNSUPPORTED
+    assert call_b(z=NULL) == _lib.FT_ERR_NULL
+    assert call_b(R1=48, U1=ALIGNED2) == _lib.FT_ERR_NULL
+    assert _lib.ft_linear_bwd_input_dgelu_workspace_size(4608, 12288, 64) == 48 * 4608 * 64 * 4
+    assert call_b(M=0) == _lib.FT_OK
