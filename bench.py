@@ -1,8 +1,9 @@
-"""Benchmark: one W4A4G4 triple-branch linear layer, forward + backward, on one GPU.
+"""Benchmark: W4A4G4 triple-branch linear layers, forward + backward, on one GPU.
 
-A step is the whole hot path over one batch of synthetic FLUX.1-dev-shaped
-input (attention QKV projection at 1024x1024: M = 4096 image + 512 text tokens,
-K = 3072, N = 9216, LoRA rank 32, stabilizer rank 32):
+The default workload (flux_qkv) is one step of the hot path over one batch of
+synthetic FLUX.1-dev-shaped input (attention QKV projection at 1024x1024:
+M = 4096 image + 512 text tokens, K = 3072, N = 9216, LoRA rank 32,
+stabilizer rank 32):
 
   quantize X (1x32 MXFP4) + P = X [L1|A]          ft_quantize_blockwise
   Y  = Q(X) Q(W)^T + P [L2;B] + bias   (bf16)      ft_linear_fwd
@@ -10,7 +11,11 @@ K = 3072, N = 9216, LoRA rank 32, stabilizer rank 32):
   dX = Q(dY) Q(W) + Qp [L1|A]^T        (bf16)      ft_linear_bwd_input
   dA = X^T (dY B^T), dB = (X A)^T dY   (fp32)      ft_lora_grads
 
-The frozen weight is quantized once before timing (offline in the method).
+Other workloads: flux_mlp (the MLP pair 3072 -> 12288 -> 3072 with the fused
+GELU / dGELU epilogues), flux_single (the single-stream block linears at batch
+4) and flux_stack (every linear of the FLUX.1-dev stack, one training step).
+
+The frozen weights are quantized once before timing (offline in the method).
 Inputs are drawn on the device with a seeded generator and are resident in HBM
 when the timed region starts.  Prints one JSON line.
 """
@@ -41,7 +46,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="flux_qkv")
+    ap.add_argument("--workload", default="flux_qkv", choices=["flux_qkv", "flux_mlp", "flux_single", "flux_stack"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="token rows in the oracle sample (0: auto)")
@@ -97,6 +102,182 @@ def copy_calibration(mib):
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}), flush=True)
 
 
+# ----------------------------------------------------------------- workloads
+# A workload is a list of layers: ("linear", M, K, N, r, r_s) runs the five
+# steps of one triple-branch linear; ("mlp", M, D, F, r, r_s) runs the MLP pair
+# D -> F -> D with the fused GELU / dGELU epilogues.  One step is every
+# layer's forward in order, then every layer's backward in reverse order.
+def workload_layers(name):
+    if name == "flux_qkv":
+        return [("linear", 4608, 3072, 9216, 32, 32)]
+    if name == "flux_mlp":
+        return [("mlp", 4608, 3072, 12288, 32, 32)]
+    if name == "flux_single":
+        return [("linear", 18432, 3072, 21504, 64, 32), ("linear", 18432, 15360, 3072, 64, 32)]
+    if name == "flux_stack":
+        layers = []
+        for _ in range(19):              # double-stream blocks: image (4096 tokens) and text (512) streams
+            for m in (4096, 512):
+                layers += [("linear", m, 3072, 9216, 32, 32), ("linear", m, 3072, 3072, 32, 32),
+                           ("mlp", m, 3072, 12288, 32, 32)]
+        for _ in range(38):              # single-stream blocks over all 4608 tokens
+            layers += [("linear", 4608, 3072, 21504, 32, 32), ("linear", 4608, 15360, 3072, 32, 32)]
+        return layers
+    raise SystemExit("unknown workload %r" % name)
+
+
+WORKLOAD_TEXT = {
+    "flux_qkv": "FLUX.1-dev attention QKV linear, batch 1 at 1024^2 (M=4608 tokens, 3072 -> 9216)",
+    "flux_mlp": "FLUX.1-dev MLP pair, batch 1 at 1024^2 (M=4608, 3072 -> 12288 -> 3072, GELU-tanh)",
+    "flux_single": "FLUX.1-dev single-stream block linears, batch 4 (M=18432: 3072 -> 21504, 15360 -> 3072)",
+    "flux_stack": "FLUX.1-dev linear stack, one training step (19 double blocks x {image 4096, text 512} tokens x "
+                  "{QKV, out, MLP pair} + 38 single blocks x {3072 -> 21504, 15360 -> 3072} at 4608 tokens)",
+}
+
+
+def linear_counts(M, K, N, r, R):
+    """(FP4 flops, low-rank flops, adapter-gradient flops, quantize bytes, adapter-gradient bytes)."""
+    fp4, lowrank, lora = layer_flops(M, K, N, r, R)
+    qbytes = M * K * (2 + 0.5 + 1 / 32) + M * R * 4 + K * R * 2 + M * N * (2 + 0.5 + 1 / 32) + M * R * 4 + N * R * 2
+    lbytes = 2.0 * M * (K + N) + 2 * M * r * 4 + 4.0 * r * (K + N)
+    return fp4, lowrank, lora, qbytes, lbytes
+
+
+class Builder:
+    """Device buffers and launch closures.  Inputs are seeded synthetic draws
+    (activations N(0,1) with 0.5% outlier channels x30, gradients 1e-3 *
+    Student-t(3), adapter and stabilizer factors N(0, 0.01^2), bias N(0,
+    0.02^2)); weights are N(0, 0.02^2) quantized once before timing, or random
+    FP4 codes and E8M0 scales for the stack (timing does not depend on values).
+    Activation buffers are shared between layers of the same shape."""
+
+    def __init__(self, torch, lib, dev, seed, random_weights):
+        self.t, self.L, self.dev = torch, lib, dev
+        self.g = torch.Generator(device=dev)
+        self.g.manual_seed(seed)
+        self.random_weights = random_weights
+        self.shared = {}
+
+    def normal(self, shape, std):
+        return (self.t.randn(shape, generator=self.g, device=self.dev) * std).to(self.t.bfloat16)
+
+    def activations(self, M, K):
+        key = ("x", M, K)
+        if key not in self.shared:
+            x = self.t.randn((M, K), generator=self.g, device=self.dev)
+            cols = self.t.randperm(K, generator=self.g, device=self.dev)[:max(1, round(0.005 * K))]
+            x[:, cols] *= 30.0
+            self.shared[key] = x.to(self.t.bfloat16)
+        return self.shared[key]
+
+    def gradient(self, M, N):
+        key = ("dy", M, N)
+        if key not in self.shared:
+            z = self.t.randn((M, N), generator=self.g, device=self.dev)
+            chi = sum(self.t.randn((M, N), generator=self.g, device=self.dev) ** 2 for _ in range(3))
+            self.shared[key] = (1e-3 * z / self.t.sqrt(chi / 3.0)).to(self.t.bfloat16)
+        return self.shared[key]
+
+    def buf(self, tag, shape, dtype):
+        key = (tag, tuple(shape), dtype)
+        if key not in self.shared:
+            self.shared[key] = self.t.empty(shape, dtype=dtype, device=self.dev)
+        return self.shared[key]
+
+    def weight(self, N, K):
+        t = self.t
+        if self.random_weights:
+            wq = t.randint(0, 256, (N, K // 2), generator=self.g, device=self.dev, dtype=t.uint8)
+            ws = t.randint(118, 124, (N // 32, K // 32), generator=self.g, device=self.dev, dtype=t.uint8)
+            return wq, ws
+        wq, ws, _ = self.L.ft_quantize_blockwise(self.normal((N, K), 0.02), block_rows=32)
+        return wq, ws
+
+    def wspace(self, nbytes):
+        return self.buf("ws%d" % nbytes, (max(nbytes, 16),), self.t.uint8)
+
+    def linear(self, M, K, N, r, rs, given=None):
+        """Closures for one linear: forward [(kind, fn)], backward [(kind, fn)],
+        counts.  `given` may supply X, dY, wq, ws, D, U, bias."""
+        t, L = self.t, self.L
+        u8, f32, bf = t.uint8, t.float32, t.bfloat16
+        R = r + rs
+        if given:
+            X, dY, wq, ws = given["X"], given["dY"], given["wq"], given["ws"]
+            D, U, bias = given["D"], given["U"], given["bias"]
+        else:
+            X, dY = self.activations(M, K), self.gradient(M, N)
+            wq, ws = self.weight(N, K)
+            D, U, bias = self.normal((K, R), 0.01), self.normal((R, N), 0.01), self.normal((N,), 0.02)
+        xq, xs = self.buf("xq", (M, K // 2), u8), self.buf("xs", (M, K // 32), u8)
+        P, Qp = self.buf("P", (M, R), f32), self.buf("Qp", (M, R), f32)
+        Y, dX = self.buf("y", (M, N), bf), self.buf("dx", (M, K), bf)
+        gq, gs = self.buf("gq", (M, N // 2), u8), self.buf("gs", (M, N // 32), u8)
+        dA, dB = self.buf("dA", (K, r), f32), self.buf("dB", (r, N), f32)
+        wx = self.wspace(L.ft_quantize_workspace_size(M, K, 1, R, L.FT_PROJ_COLS_BY_R))
+        wd = self.wspace(L.ft_quantize_workspace_size(M, N, 1, R, L.FT_PROJ_R_BY_COLS))
+        wl = self.wspace(L.ft_lora_grads_workspace_size(M, K, N, R, r))
+        fwd = [("quantize_x", lambda: L.ft_quantize_blockwise(X, proj=D, codes=xq, scales=xs, proj_out=P, workspace=wx)),
+               ("gemm_fwd", lambda: L.ft_linear_fwd(xq, xs, wq, ws, K, P, U, bias, y=Y))]
+        bwd = [("quantize_dy", lambda: L.ft_quantize_blockwise(dY, proj=U, proj_layout=L.FT_PROJ_R_BY_COLS, codes=gq,
+                                                              scales=gs, proj_out=Qp, workspace=wd)),
+               ("gemm_bwd", lambda: L.ft_linear_bwd_input(gq, gs, wq, ws, K, Qp, D, dx=dX)),
+               ("lora_grads", lambda: L.ft_lora_grads(X, dY, P, Qp, r, col0=rs, dA=dA, dB=dB, workspace=wl))]
+        fp4, lowrank, lora, qb, lb = linear_counts(M, K, N, r, R)
+        counts = {"flops": fp4 + lowrank + lora, "gemm_fwd": fp4 / 2, "gemm_bwd": fp4 / 2,
+                  "quantize_x": M * K * (2 + 0.5 + 1 / 32) + M * R * 4 + K * R * 2,
+                  "quantize_dy": M * N * (2 + 0.5 + 1 / 32) + M * R * 4 + N * R * 2, "lora_grads": lb}
+        return fwd, bwd, counts
+
+    def mlp(self, M, Dm, F, r, rs):
+        """MLP pair Dm -> F -> Dm: FC1 forward fused with GELU and FC2's input
+        preparation, FC2 backward-input fused with dGELU and FC1's gradient
+        preparation."""
+        t, L = self.t, self.L
+        u8, f32, bf = t.uint8, t.float32, t.bfloat16
+        R = r + rs
+        X, dY = self.activations(M, Dm), self.gradient(M, Dm)
+        w1q, w1s = self.weight(F, Dm)
+        w2q, w2s = self.weight(Dm, F)
+        D1, U1, b1 = self.normal((Dm, R), 0.01), self.normal((R, F), 0.01), self.normal((F,), 0.02)
+        D2, U2, b2 = self.normal((F, R), 0.01), self.normal((R, Dm), 0.01), self.normal((Dm,), 0.02)
+        xq, xs = self.buf("xq", (M, Dm // 2), u8), self.buf("xs", (M, Dm // 32), u8)
+        P1, P2 = self.buf("P1", (M, R), f32), self.buf("P2", (M, R), f32)
+        Qp1, Qp2 = self.buf("Qp1", (M, R), f32), self.buf("Qp2", (M, R), f32)
+        z, h = self.buf("z", (M, F), bf), self.buf("h", (M, F), bf)
+        hq, hs = self.buf("hq", (M, F // 2), u8), self.buf("hs", (M, F // 32), u8)
+        Y = self.buf("y", (M, Dm), bf)
+        gq, gs = self.buf("gq", (M, Dm // 2), u8), self.buf("gs", (M, Dm // 32), u8)
+        dz = self.buf("dz", (M, F), bf)
+        dzq, dzs = self.buf("dzq", (M, F // 2), u8), self.buf("dzs", (M, F // 32), u8)
+        dX = self.buf("dx", (M, Dm), bf)
+        dA1, dB1 = self.buf("dA1", (Dm, r), f32), self.buf("dB1", (r, F), f32)
+        dA2, dB2 = self.buf("dA2", (F, r), f32), self.buf("dB2", (r, Dm), f32)
+        wx = self.wspace(L.ft_quantize_workspace_size(M, Dm, 1, R, L.FT_PROJ_COLS_BY_R))
+        wd = self.wspace(L.ft_quantize_workspace_size(M, Dm, 1, R, L.FT_PROJ_R_BY_COLS))
+        wg = self.wspace(L.ft_linear_fwd_gelu_workspace_size(M, F, R))
+        wdg = self.wspace(L.ft_linear_bwd_input_dgelu_workspace_size(M, F, R))
+        wl1 = self.wspace(L.ft_lora_grads_workspace_size(M, Dm, F, R, r))
+        wl2 = self.wspace(L.ft_lora_grads_workspace_size(M, F, Dm, R, r))
+        fwd = [("quantize_x", lambda: L.ft_quantize_blockwise(X, proj=D1, codes=xq, scales=xs, proj_out=P1, workspace=wx)),
+               ("gemm_fwd_gelu", lambda: L.ft_linear_fwd_gelu(xq, xs, w1q, w1s, Dm, P1, U1, b1, D2=D2, z=z, h=h,
+                                                               hq=hq, hs=hs, P2=P2, workspace=wg)),
+               ("gemm_fwd", lambda: L.ft_linear_fwd(hq, hs, w2q, w2s, F, P2, U2, b2, y=Y))]
+        bwd = [("quantize_dy", lambda: L.ft_quantize_blockwise(dY, proj=U2, proj_layout=L.FT_PROJ_R_BY_COLS, codes=gq,
+                                                              scales=gs, proj_out=Qp2, workspace=wd)),
+               ("gemm_bwd_dgelu", lambda: L.ft_linear_bwd_input_dgelu(gq, gs, w2q, w2s, F, z, Qp2, D2, U1=U1, dz=dz,
+                                                                       dzq=dzq, dzs=dzs, Qp1=Qp1, workspace=wdg)),
+               ("gemm_bwd", lambda: L.ft_linear_bwd_input(dzq, dzs, w1q, w1s, Dm, Qp1, D1, dx=dX)),
+               ("lora_grads", lambda: L.ft_lora_grads(h, dY, P2, Qp2, r, col0=rs, dA=dA2, dB=dB2, workspace=wl2)),
+               ("lora_grads", lambda: L.ft_lora_grads(X, dz, P1, Qp1, r, col0=rs, dA=dA1, dB=dB1, workspace=wl1))]
+        c1, c2 = linear_counts(M, Dm, F, r, R), linear_counts(M, F, Dm, r, R)
+        counts = {"flops": sum(c1[:3]) + sum(c2[:3]),
+                  "gemm_fwd_gelu": c1[0] / 2, "gemm_fwd": c2[0] / 2, "gemm_bwd_dgelu": c2[0] / 2, "gemm_bwd": c1[0] / 2,
+                  "quantize_x": M * Dm * (2 + 0.5 + 1 / 32) + M * R * 4 + Dm * R * 2,
+                  "quantize_dy": M * Dm * (2 + 0.5 + 1 / 32) + M * R * 4 + Dm * R * 2, "lora_grads": c1[4] + c2[4]}
+        return fwd, bwd, counts
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -115,45 +296,34 @@ def main():
     _lib.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    shape = gen.SHAPES[args.workload]
-    M, K, N, r, rs, R = shape.M, shape.K, shape.N, shape.r, shape.r_s, shape.R
-
-    d = gen.layer_inputs_torch(shape, args.seed, dev)
-    X, W, D, U, dY, bias = d["X"], d["W"], d["D"], d["U"], d["dY"], d["bias"]
-    wq, ws, _ = _lib.ft_quantize_blockwise(W, block_rows=32)            # offline weight preparation
-    u8, f32, bf = torch.uint8, torch.float32, torch.bfloat16
-    xq = torch.empty((M, K // 2), dtype=u8, device=dev); xs = torch.empty((M, K // 32), dtype=u8, device=dev)
-    P = torch.empty((M, R), dtype=f32, device=dev)
-    Y = torch.empty((M, N), dtype=bf, device=dev)
-    gq = torch.empty((M, N // 2), dtype=u8, device=dev); gs = torch.empty((M, N // 32), dtype=u8, device=dev)
-    Qp = torch.empty((M, R), dtype=f32, device=dev)
-    dX = torch.empty((M, K), dtype=bf, device=dev)
-    dA = torch.empty((K, r), dtype=f32, device=dev); dB = torch.empty((r, N), dtype=f32, device=dev)
-    # workspaces for the partial sums (allocated once, outside the timed region)
-    wspace = lambda n: torch.empty(max(n, 16), dtype=u8, device=dev)
-    ws_x = wspace(_lib.ft_quantize_workspace_size(M, K, 1, R, _lib.FT_PROJ_COLS_BY_R))
-    ws_dy = wspace(_lib.ft_quantize_workspace_size(M, N, 1, R, _lib.FT_PROJ_R_BY_COLS))
-    ws_lg = wspace(_lib.ft_lora_grads_workspace_size(M, K, N, R, r))
-
-    names = ["quantize_x", "gemm_fwd", "quantize_dy", "gemm_bwd", "lora_grads"]
+    layers = workload_layers(args.workload)
+    b = Builder(torch, _lib, dev, args.seed, random_weights=args.workload == "flux_stack")
+    fwd_ops, bwd_ops, counts = [], [], {}
+    d = given = None
+    if args.workload == "flux_qkv":
+        # the headline layer keeps the seeded recipe of the parity tests
+        d = gen.layer_inputs_torch(gen.SHAPES["flux_qkv"], args.seed, dev)
+        wq, ws, _ = _lib.ft_quantize_blockwise(d["W"], block_rows=32)     # offline weight preparation
+        given = dict(X=d["X"], dY=d["dY"], wq=wq, ws=ws, D=d["D"], U=d["U"], bias=d["bias"])
+    for kind, M, K, N, r, rs in layers:
+        if kind == "linear":
+            f, bw, c = b.linear(M, K, N, r, rs, given)
+        else:
+            f, bw, c = b.mlp(M, K, N, r, rs)
+        fwd_ops.append(f)
+        bwd_ops.append(bw)
+        for k, v in c.items():
+            counts[k] = counts.get(k, 0.0) + v
+    ops = [op for f in fwd_ops for op in f] + [op for bw in reversed(bwd_ops) for op in bw]
+    torch.cuda.synchronize()
 
     def step(ev=None):
-        def mark(i):
+        for i, (_, fn) in enumerate(ops):
             if ev is not None:
                 ev[i].record()
-        mark(0)
-        _lib.ft_quantize_blockwise(X, proj=D, proj_layout=_lib.FT_PROJ_COLS_BY_R, codes=xq, scales=xs, proj_out=P,
-                                   workspace=ws_x)
-        mark(1)
-        _lib.ft_linear_fwd(xq, xs, wq, ws, K, P, U, bias, y=Y)
-        mark(2)
-        _lib.ft_quantize_blockwise(dY, proj=U, proj_layout=_lib.FT_PROJ_R_BY_COLS, codes=gq, scales=gs, proj_out=Qp,
-                                   workspace=ws_dy)
-        mark(3)
-        _lib.ft_linear_bwd_input(gq, gs, wq, ws, K, Qp, D, dx=dX)
-        mark(4)
-        _lib.ft_lora_grads(X, dY, P, Qp, r, col0=rs, dA=dA, dB=dB, workspace=ws_lg)
-        mark(5)
+            fn()
+        if ev is not None:
+            ev[len(ops)].record()
 
     for _ in range(args.warmup):
         step()
@@ -169,27 +339,40 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = t0.elapsed_time(t1) / args.steps
 
-    # per-kernel timing: events around each launch, same stream
-    per = {n: [] for n in names}
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
-    for s in range(args.steps):
-        step(evs[s])
+    # per-kernel timing: events around each call, same stream (a few steps)
+    psteps = min(args.steps, 20 if len(ops) < 50 else 2)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)] for _ in range(psteps)]
+    for s_ in range(psteps):
+        step(evs[s_])
     torch.cuda.synchronize()
-    for s in range(args.steps):
-        for i, n in enumerate(names):
-            per[n].append(evs[s][i].elapsed_time(evs[s][i + 1]))
-    avg_us = {n: 1e3 * sum(v) / len(v) for n, v in per.items()}
+    kinds = []
+    for k, _ in ops:
+        if k not in kinds:
+            kinds.append(k)
+    tot_us = {k: 0.0 for k in kinds}
+    calls = {k: 0 for k in kinds}
+    for s_ in range(psteps):
+        for i, (k, _) in enumerate(ops):
+            tot_us[k] += 1e3 * evs[s_][i].elapsed_time(evs[s_][i + 1])
+            calls[k] += 1
+    step_us = {k: tot_us[k] / psteps for k in kinds}          # per step, summed over the step's calls
+    launch_us = {k: tot_us[k] / calls[k] for k in kinds}     # per call
 
-    fp4, lowrank, lora = layer_flops(M, K, N, r, R)
-    total = fp4 + lowrank + lora
-    tflops = total / (ms_per_step * 1e-3) / 1e12
-
-    gemm = max(("gemm_fwd", "gemm_bwd"), key=lambda n: avg_us[n])
-    gemm_flops = 2.0 * M * N * K
-    achieved = gemm_flops / (avg_us[gemm] * 1e-6) / 1e12
-    quant_bytes = M * K * (2 + 0.5 + 1 / 32) + M * R * 4 + K * R * 2
-    qdy_bytes = M * N * (2 + 0.5 + 1 / 32) + M * R * 4 + N * R * 2
-    lora_bytes = 2.0 * M * (K + N) + 2 * M * r * 4 + 4.0 * r * (K + N)
+    tflops = counts["flops"] / (ms_per_step * 1e-3) / 1e12
+    gemms = [k for k in kinds if k.startswith("gemm")]
+    gemm = max(gemms, key=lambda k: step_us[k])
+    per_call_flops = counts[gemm] / (calls[gemm] / psteps)
+    achieved = counts[gemm] / (step_us[gemm] * 1e-6) / 1e12
+    kname = {"gemm_fwd": "ft::k_gemm_fp4_pipe<false, false, 0> (forward)",
+             "gemm_bwd": "ft::k_gemm_fp4_pipe<true, false, 0> (backward-input)",
+             "gemm_fwd_gelu": "ft::k_gemm_fp4_pipe<false, false, 1> (forward, GELU epilogue)",
+             "gemm_bwd_dgelu": "ft::k_gemm_fp4_pipe<true, false, 2> (backward-input, dGELU epilogue)"}[gemm]
+    frac = {}
+    for k in kinds:
+        if k.startswith("gemm"):
+            frac[k + "_mxfp4"] = round(counts[k] / (step_us[k] * 1e-6) / 1e12 / MXFP4_PEAK_TFLOPS, 4)
+        else:
+            frac[k + "_hbm"] = round(counts[k] / (step_us[k] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
 
     out = {
         "metric": "fused W4A4 linear fwd+bwd TFLOP/s at FLUX 1024^2 shapes; % MXFP4 MFMA peak",
@@ -204,26 +387,26 @@ def main():
         "vs_baseline": None,
         "dtype": "mxfp4",
         "data": "synthetic",
-        "config": {"workload": "FLUX.1-dev attention QKV linear, batch 1 at 1024^2 (%s)" % shape.name,
-                   "M": M, "K": K, "N": N, "lora_rank": r, "stabilizer_rank": rs,
-                   "outputs": "Y, dX bf16; dA, dB fp32", "parallelism": "single GPU"},
+        "config": {"workload": "%s: %s" % (args.workload, WORKLOAD_TEXT[args.workload]),
+                   "layers": len(layers), "lora_rank": layers[0][4], "stabilizer_rank": layers[0][5],
+                   "outputs": "activations and input gradients bf16; dA, dB fp32", "parallelism": "single GPU"},
         "pct_mxfp4_peak": round(100.0 * tflops / MXFP4_PEAK_TFLOPS, 2),
-        "roofline": {"bound": "mfma", "kernel": "ft::k_gemm_fp4_pipe<%s> (%s)" % (("true, false", "backward-input") if gemm == "gemm_bwd" else ("false, false", "forward")),
+        "roofline": {"bound": "mfma", "kernel": kname,
                      "achieved": round(achieved, 1), "peak": MXFP4_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / MXFP4_PEAK_TFLOPS, 4),
-                     "traffic": measured_traffic("bwd" if gemm == "gemm_bwd" else "fwd"),
-                     "per_launch_flops": gemm_flops, "avg_launch_us": round(avg_us[gemm], 2)},
-        "kernels_us": {n: round(v, 2) for n, v in avg_us.items()},
-        "kernels_frac": {
-            "gemm_fwd_mxfp4": round(gemm_flops / (avg_us["gemm_fwd"] * 1e-6) / 1e12 / MXFP4_PEAK_TFLOPS, 4),
-            "gemm_bwd_mxfp4": round(gemm_flops / (avg_us["gemm_bwd"] * 1e-6) / 1e12 / MXFP4_PEAK_TFLOPS, 4),
-            "quantize_x_hbm": round(quant_bytes / (avg_us["quantize_x"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
-            "quantize_dy_hbm": round(qdy_bytes / (avg_us["quantize_dy"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
-            "lora_grads_hbm": round(lora_bytes / (avg_us["lora_grads"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
-        },
+                     "traffic": measured_traffic("bwd" if gemm == "gemm_bwd" else "fwd")
+                     if args.workload == "flux_qkv" else None,
+                     "per_launch_flops": per_call_flops, "avg_launch_us": round(launch_us[gemm], 2)},
+        "kernels_us": {k: round(step_us[k], 2) for k in kinds},
+        "kernels_frac": frac,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(d, shape, args.cpu_rows)
+        if d is None:
+            shape = gen.SHAPES["flux_qkv"]
+            d = gen.layer_inputs_torch(shape, args.seed, dev)
+        out["cpu_baseline"] = cpu_baseline(d, gen.SHAPES["flux_qkv"], args.cpu_rows)
+        if args.workload != "flux_qkv":
+            out["cpu_baseline"]["sample"] += " (the QKV linear, the oracle's per-linear rate)"
     print(json.dumps(out), flush=True)
 
 

@@ -80,7 +80,7 @@ struct GeluParts { float one_plus_t, one_minus_t2; };
 __device__ __forceinline__ GeluParts gelu_parts(float z) {
   const float u = kGeluC0 * (z + kGeluC1 * z * z * z);
   const float e = __builtin_amdgcn_exp2f(-2.8853900817779268f * fabsf(u));   // exp(-2|u|)
-  const float r = 1.0f / (1.0f + e);
+  const float r = __builtin_amdgcn_rcpf(1.0f + e);   // hardware reciprocal (1 ulp)
   return {(u >= 0.0f ? 2.0f : 2.0f * e) * r, 4.0f * e * r * r};
 }
 __device__ __forceinline__ float gelu_tanh(float z) { return 0.5f * z * gelu_parts(z).one_plus_t; }

@@ -820,6 +820,19 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     const __amdgpu_buffer_rsrc_t r_q = make_rsrc(ep.q, (uint32_t)M * (NO / 2));
     const int g16 = lane >> 4, t16 = lane & 15, jj = t16 >> 2, qq = t16 & 3;
     const int rt2 = (R2 + 31) >> 5;
+    // EPI_DGELU: every z segment this lane needs, loaded before the first
+    // store (a load waited for after stores would wait for those stores too)
+    v4i zpre[4][8];
+    if constexpr (!G) {
+#pragma unroll
+      for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int it = 0; it < 8; it++) {
+          const int gr = orow0 + 32 * i + 4 * it + g16, gc = ocol0 + 8 * t16;
+          zpre[i][it] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+              r_z, (gr < M && gc < NO) ? ((uint32_t)gr * NO + gc) * 2 : kOobOffset, 0, 0));
+        }
+    }
 #pragma unroll   // acc[i] must be indexed by constants
     for (int i = 0; i < 4; i++) {
       // 1) stage this pass's 32 rows
@@ -840,8 +853,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
           }
         }
       __builtin_amdgcn_s_waitcnt(0xc07f);
+      if constexpr (!G) {
+        if (i == 0) wait_vm<0>();   // z arrived (no store issued yet)
+      }
       // 2) row segments: outputs, block codes, bf16 result back in place
-#pragma unroll 2
+#pragma unroll
       for (int it = 0; it < 8; it++) {
         const int rl = 4 * it + g16, seg = t16;
         const int gr = orow0 + 32 * i + rl, gc = ocol0 + 8 * seg;
@@ -859,7 +875,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
           }
         } else {
           const float4 d0 = *(const float4*)(srow + seg * 32), d1 = *(const float4*)(srow + seg * 32 + 16);
-          const v4i zb = __builtin_amdgcn_raw_buffer_load_b128(r_z, off2, 0, 0);
+          const v4i zb = zpre[i][it];
           const float dh[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
 #pragma unroll
           for (int e = 0; e < 4; e++) {
