@@ -295,3 +295,26 @@ def test_layer_flux_qkv_full_size_sampled():
     dA, dB, _, _ = ref.lora_grads(d["X"], d["dY"], Pf[:, rs:], Qf[:, rs:], want_s=False)
     assert np.linalg.norm(g["dA"] - dA) <= 1e-3 * np.linalg.norm(dA)
     assert np.linalg.norm(g["dB"] - dB) <= 1e-3 * np.linalg.norm(dB)
+
+
+@pytest.mark.parametrize("name", ["flux_single_linear1", "flux_single_linear2"])
+def test_layer_flux_single_stream_full_size_sampled(name):
+    """FLUX.1-dev single-stream block linears at batch 4 (M = 18432 tokens;
+    3072 -> 21504 and 15360 -> 3072; LoRA rank 64, stabilizer rank 32), as in
+    the stack step: quantized operands and adapter gradients in full, GEMM
+    outputs on sampled rows."""
+    shape = gen.SHAPES[name]
+    d = make_case(shape, 4)
+    g = run_gpu_layer(d, shape)
+    rows = np.array([0, 255, 256, 5000, 9999, 18175, 18431])
+    xq, xs = ref.quantize(d["X"], 1)
+    assert np.array_equal(g["xq"], xq) and np.array_equal(g["xs"], xs)
+    gq, gs = ref.quantize(d["dY"], 1)
+    assert np.array_equal(g["gq"], gq) and np.array_equal(g["gs"], gs)
+    check_layer(d, shape, g, rows=rows)
+    rs = shape.r_s
+    Pf, _ = ref.proj(d["X"], d["D"], 0)
+    Qf, _ = ref.proj(d["dY"], d["U"], 1)
+    dA, dB, _, _ = ref.lora_grads(d["X"], d["dY"], Pf[:, rs:], Qf[:, rs:], want_s=False)
+    assert np.linalg.norm(g["dA"] - dA) <= 1e-3 * np.linalg.norm(dA)
+    assert np.linalg.norm(g["dB"] - dB) <= 1e-3 * np.linalg.norm(dB)
