@@ -229,13 +229,15 @@ __device__ __forceinline__ void wait_vm() {
 // buffer size reads zeros whatever soff is.
 // The uniform operands pass through readfirstlane: the compiler may hold a
 // uniform value in a VGPR, which an "s" asm operand would not convert.
+// An LDS DMA needs one wait state after a scalar write of M0 (the compiler
+// inserts it for the loads it generates, not inside an asm block).
 __device__ __forceinline__ void dma16(v4i rsrc, uint32_t lds_base, uint32_t voff, uint32_t soff) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc),
                   "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
 }
 __device__ __forceinline__ void dma4(v4i rsrc, uint32_t lds_base, uint32_t voff, uint32_t soff) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, %3 offen lds"
                :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc),
                   "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
 }

@@ -229,32 +229,45 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_generic(const uint8_t* __re
 
 // ============================================================== fast path
 // Pipelined kernel for reduction lengths that are multiples of 128 (and, for
-// the backward, K a multiple of 128).  Every stage of work moves through a
-// 4-slot LDS ring with buffer loads that write LDS directly; rows past the
+// the backward, K a multiple of 128).  Stages of work move through a 2-slot
+// LDS ring filled by buffer loads that write LDS directly; rows past the
 // matrix edge read as zeros through the buffer range check, so tiles need no
-// branches.  Three stages are in flight while one runs on the matrix cores.
+// branches.
 //
 // Stage kinds:
-//   FP4 stage: 128 reduction elements.  Slot = A tile [256 rows][64 B] +
-//     W tile (forward [256 n][64 B]; backward [128 n][128 B], read with the
-//     nibble-transposing LDS read) + the stage's E8M0 scales.
-//   Low-rank stage (after the FP4 stages): 16 columns of the up-projection.
-//     Slot = P chunk [256 rows][16 fp32] + U chunk (forward, [16 j][256 n]
-//     bf16) or D chunk (backward, [256 k][16 j] bf16).  P is split into two
+//   FP4 stage: 256 reduction elements, so that each tile row of a stage is one
+//     whole 128-byte line: what the loads cost follows the number of lines
+//     they touch more than their bytes.  Slot = A tile [256 rows][128 B] +
+//     W tile (forward [256 n][128 B]; backward [256 reduction rows][128 B],
+//     read with the nibble-transposing LDS read) + the stage's E8M0 scales.
+//     When the reduction length is an odd multiple of 128, the upper half of
+//     the last stage reads as zeros.
+//   Low-rank stage (after the FP4 stages): 32 columns of the up-projection.
+//     Slot = P chunk [256 rows][32 fp32] + U chunk (forward, [32 j][256 n]
+//     bf16) or D chunk (backward, [256 k][32 j] bf16).  P is split into two
 //     bf16 terms in registers; its product lands in the same accumulators.
-// Within a stage, the barrier that publishes the next stage sits between the
-// two k-steps, so the next stage's first fragments load under the current
-// MFMAs.  The finished tile is staged through LDS for coalesced stores.
+// An FP4 stage runs as four k-steps of 16 MFMAs per wave (a low-rank stage
+// as two of 32), each carrying the LDS reads of the next.  Stage s+2 loads in
+// two parts: the first right after the barrier that publishes stage s+1 (the
+// slot of stage s is free from then on), the second during the first k-step
+// of stage s+1; the barrier before the last k-step of stage s+1 publishes it.
+// The finished tile is staged through LDS for coalesced stores.
 
-constexpr int PK = 128;                  // reduction elements per FP4 stage
-constexpr int PROW = PK / 2;             // bytes per A-tile row per stage
-constexpr int SLOT = 36 * 1024;          // bytes per ring slot
-constexpr int NSLOT = 4;
-constexpr int OFF_B = 16 * 1024;         // W tile / U / D chunk within a slot
-constexpr int OFF_SA = 32 * 1024;        // A scales: 256 rows x 4 bytes
-constexpr int OFF_SB = 33 * 1024;        // W scales: 4 waves x 256 bytes
-constexpr int LOADS_FP4 = 10;            // buffer loads per wave per FP4 stage
-constexpr int LOADS_LR = 6;              // ... per low-rank stage
+constexpr int PK = 256;                  // reduction elements per FP4 stage
+constexpr int PROW = PK / 2;             // bytes per tile row per stage (one line)
+constexpr int SLOT = 68 * 1024;          // bytes per ring slot
+constexpr int NSLOT = 2;
+constexpr int OFF_B = 32 * 1024;         // W tile / U / D chunk within a slot
+constexpr int OFF_SA = 64 * 1024;        // A scales: 256 rows x 8 bytes
+constexpr int OFF_SB = 66 * 1024;        // W scales: 4 waves x 256 bytes
+constexpr int LR_COLS = 32;              // up-projection columns per low-rank stage
+// buffer loads per wave in the first part of a stage: FP4 (A tile, A scales), low-rank (P chunk)
+constexpr int LOADS_A = 10;
+constexpr int LOADS_P = 8;
+
+// Stage kinds, and a compile-time tag for the pipeline bodies.
+enum { SK_NONE = 0, SK_FP4 = 1, SK_LR = 2 };
+template <int V> struct IC { static constexpr int value = V; };
 
 // 16-byte chunk swizzles: 64-byte rows (4 chunks) and 128-byte rows (8 chunks)
 __device__ __forceinline__ int swz64(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
@@ -305,7 +318,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   const v4i rl = rsrc_words(LR, (uint32_t)(BWD ? K : N) * R * 2);
   const uint32_t lds0 = lds_addr(lds);
 
-  const int nst = KR / PK, nlr = R / 16, total = nst + nlr;
+  const int nst = (KR + PK - 1) / PK;            // FP4 stages
+  const int nfull = KR / PK;                     // ... of which whole (the last may be half)
+  const bool half_last = nfull != nst;
+  const int nlr = (R + LR_COLS - 1) / LR_COLS, total = nst + nlr;
+  const bool half_lr = (R % LR_COLS) != 0;       // the last low-rank stage has 16 columns
 
   // Accumulator tiles are computed transposed (W fragment as MFMA operand A):
   // lane (r32, h) of tile acc[i][j] holds output row wm*128 + 32i + r32 and,
@@ -324,159 +341,246 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     }
 
   // ---------------- per-lane load geometry (constant over stages)
-  // Each buffer load takes a per-lane byte offset (constant over stages; rows
-  // outside the matrix hold kOobOffset, which reads zeros) plus a uniform
-  // per-stage offset.
-  // 64-byte-row tiles (A, forward W, P chunk): instruction i of this wave
-  // fills rows wave*64 + 16i + [0,16); lane L -> row + L/4, chunk (L%4)^swz64.
-  const int r64 = wave * 64 + (lane >> 2);
-  const int c64 = (lane & 3) ^ swz64(lane >> 2);
-  uint32_t a_base[4], w_base[4], p_base[4];
+  // Each buffer load takes a per-lane byte offset (rows outside the matrix
+  // hold kOobOffset, which reads zeros) plus a uniform per-stage offset that
+  // stays inside the row of every valid lane.
+  // 128-byte-row tiles (A, W, P chunk): instruction u of this wave fills rows
+  // wave*64 + 8u + [0,8); lane L -> row + L/8 and physical chunk L%8, which
+  // holds logical chunk (L%8) ^ swz128(row) = c8 ^ (u & 1).
+  const int r8 = lane >> 3;
+  const int c8 = (lane & 7) ^ r8;
+  const bool upper = (c8 & 4) != 0;              // logical chunks 4..7 (the upper half of a stage)
+  uint32_t a_base[8], w_base[8];
 #pragma unroll
-  for (int i = 0; i < 4; i++) {
-    const int r = r64 + 16 * i;
-    a_base[i] = (m0 + r < M) ? (uint32_t)(m0 + r) * lda + c64 * 16 : kOobOffset;
-    p_base[i] = (m0 + r < M) ? (uint32_t)(m0 + r) * R * 4 + c64 * 16 : kOobOffset;
-    w_base[i] = kOobOffset;
-    if constexpr (!BWD) w_base[i] = (n0 + r < N) ? (uint32_t)(n0 + r) * ldw + c64 * 16 : kOobOffset;
+  for (int u = 0; u < 8; u++) {
+    const int r = wave * 64 + 8 * u + r8;
+    const int c = c8 ^ (u & 1);
+    a_base[u] = (m0 + r < M) ? (uint32_t)(m0 + r) * lda + c * 16 : kOobOffset;
+    if constexpr (!BWD) {
+      w_base[u] = (n0 + r < N) ? (uint32_t)(n0 + r) * ldw + c * 16 : kOobOffset;
+    } else {
+      // reduction row r of the stage; the tile's 256 output columns are 128 bytes of it
+      const int byte = (n0 >> 1) + c * 16;
+      w_base[u] = (byte < ldw) ? (uint32_t)r * ldw + byte : kOobOffset;
+    }
   }
-  // backward W tile: 128 reduction rows x 128 bytes; instruction i fills rows
-  // wave*32 + 8i + [0,8); lane L -> row + L/8, chunk (L%8) ^ swz128(row).
-  const int rb128 = wave * 32 + (lane >> 3);
-  const int cb128 = (lane & 7) ^ swz128(lane >> 3);
-  uint32_t wt_base[4];
+  // A scales: instruction v of wave w stages rows wave*64 + 32v + L/2, dword
+  // L%2 (blocks 4(L%2)..+3 of the stage) at OFF_SA + 8*row + 4(L%2).
+  uint32_t sa_base[2];
 #pragma unroll
-  for (int i = 0; i < 4; i++) {
-    const int byte = (n0 >> 1) + ((cb128 ^ (i & 1)) * 16);
-    wt_base[i] = (byte < ldw) ? (uint32_t)(rb128 + 8 * i) * ldw + byte : kOobOffset;
+  for (int v = 0; v < 2; v++) {
+    const int r = m0 + wave * 64 + 32 * v + (lane >> 1);
+    sa_base[v] = (r < M) ? (uint32_t)r * nkb + 4 * (lane & 1) : kOobOffset;
   }
-  // scales: wave w stages A-scale dwords of tile rows 64w + lane; W scales:
-  //   forward: lanes 0,1 of wave w fetch 32-column blocks 2w, 2w+1 of the tile;
-  //   backward: lanes 0,1 of wave w fetch W-scale row (stage*4 + w), blocks 4*lane..+3.
-  const uint32_t sa_base = (m0 + wave * 64 + lane < M) ? (uint32_t)(m0 + wave * 64 + lane) * nkb : kOobOffset;
+  // W scales (lanes 0..3 of each wave, two 8-byte rows per wave):
+  //   forward: 32-column block 2w + L/2 of the tile, dword L%2 of the stage;
+  //   backward: reduction block 2w + L/2 of the stage, dword L%2 (column
+  //   blocks 4(L%2)..+3 of the tile).
+  // Row b lands at OFF_SB + (b/2)*256 + (b%2)*8 (each wave writes its own 256 bytes).
   uint32_t sb_base = kOobOffset;
-  if (lane < 2) {
+  if (lane < 4) {
+    const int b = 2 * wave + (lane >> 1), d = lane & 1;
     if constexpr (!BWD) {
-      const int nb = (n0 >> 5) + 2 * wave + lane;
-      if (nb < (N >> 5)) sb_base = (uint32_t)nb * nwkb;
+      const int nb = (n0 >> 5) + b;
+      if (nb < (N >> 5)) sb_base = (uint32_t)nb * nwkb + 4 * d;
     } else {
-      const int kb = (n0 >> 5) + 4 * lane;
-      if (kb < (K >> 5)) sb_base = (uint32_t)wave * nwkb + kb;
+      const int kb = (n0 >> 5) + 4 * d;
+      if (kb < nwkb) sb_base = (uint32_t)b * nwkb + kb;
     }
   }
-  // low-rank chunk geometry
-  //   forward U chunk [16 j][256 n] (512-byte rows): instruction i fills rows
-  //     2i, 2i+1 (waves 0..3 own instructions 2w, 2w+1); lane L -> row + L/32,
-  //     chunk (L%32) ^ (2*(row&3)).
-  //   backward D chunk [256 k][16 j] (32-byte rows): instruction i fills rows
-  //     32i + [0,32) (waves own 2w, 2w+1); lane L -> row + L/2, half (L%2)^((row>>2)&1).
-  uint32_t l_base[2];
-#pragma unroll
-  for (int i = 0; i < 2; i++) {
-    const int ins = 2 * wave + i;
-    if constexpr (!BWD) {
-      const int j = 2 * ins + (lane >> 5);
-      const int c = (lane & 31) ^ (2 * (j & 3));
-      l_base[i] = (n0 + c * 8 < N) ? (uint32_t)j * N * 2 + (uint32_t)(n0 + c * 8) * 2 : kOobOffset;
-    } else {
-      const int k = 32 * ins + (lane >> 1);
-      const int c = (lane & 1) ^ ((k >> 2) & 1);
-      l_base[i] = (n0 + k < K) ? (uint32_t)(n0 + k) * R * 2 + c * 16 : kOobOffset;
-    }
-  }
-
   auto slot_of = [&](int t) { return (uint32_t)((t & (NSLOT - 1)) * SLOT); };
+  auto kind_of = [&](int u) { return u >= total ? SK_NONE : (u < nst ? SK_FP4 : SK_LR); };
 
   // ---------------- stage loads (LDS destinations and per-stage offsets are uniform)
-  auto issue_fp4 = [&](int t) {
-    const uint32_t slot = lds0 + slot_of(t);
-    const uint32_t sa_off = (uint32_t)t * PROW;
-#pragma unroll
-    for (int i = 0; i < 4; i++) dma16(ra, slot + (wave * 64 + 16 * i) * PROW, a_base[i], sa_off);
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-      if constexpr (!BWD) dma16(rw, slot + OFF_B + (wave * 64 + 16 * i) * PROW, w_base[i], sa_off);
-      else dma16(rw, slot + OFF_B + (wave * 32 + 8 * i) * 128, wt_base[i], (uint32_t)t * PK * ldw);
+  // One load at a time, so that loads can sit between MFMAs.  hf: the stage
+  // is a half one (FP4: upper 128 reduction elements; low-rank: 16 columns),
+  // whose missing part reads as zeros.
+  // FP4 stage u, part 1: loads v < 8 fill A-tile rows wave*64 + 8v + [0,8);
+  // v = 8, 9 stage A-scale rows wave*64 + 32(v-8) + [0,32).
+  auto fp4_part1_one = [&](int u, int v, bool hf) {
+    const uint32_t slot = lds0 + slot_of(u);
+    if (v < 8)
+      dma16(ra, slot + (wave * 64 + 8 * v) * PROW, (hf && upper) ? kOobOffset : a_base[v], (uint32_t)u * PROW);
+    else
+      dma4(ras, slot + OFF_SA + (wave * 64 + 32 * (v - 8)) * 8, (hf && (lane & 1)) ? kOobOffset : sa_base[v - 8],
+           (uint32_t)u * 8);
+  };
+  // FP4 stage u, part 2: loads v < 8 fill W-tile rows wave*64 + 8v + [0,8);
+  // v = 8 stages this wave's two W-scale rows.
+  auto fp4_part2_one = [&](int u, int v, bool hf) {
+    const uint32_t slot = lds0 + slot_of(u);
+    if constexpr (!BWD) {
+      if (v < 8)
+        dma16(rw, slot + OFF_B + (wave * 64 + 8 * v) * PROW, (hf && upper) ? kOobOffset : w_base[v],
+              (uint32_t)u * PROW);
+      else
+        dma4(rws, slot + OFF_SB + wave * 256, (hf && (lane & 1)) ? kOobOffset : sb_base, (uint32_t)u * 8);
+    } else {
+      // rows 128..255 of a half stage (waves 2, 3) are past the matrix
+      const bool off = hf && wave >= 2;
+      if (v < 8)
+        dma16(rw, slot + OFF_B + (wave * 64 + 8 * v) * 128, off ? kOobOffset : w_base[v], (uint32_t)u * PK * ldw);
+      else
+        dma4(rws, slot + OFF_SB + wave * 256, off ? kOobOffset : sb_base, (uint32_t)u * 8 * nwkb);
     }
-    dma4(ras, slot + OFF_SA + wave * 256, sa_base, (uint32_t)t * 4);
-    if constexpr (!BWD) dma4(rws, slot + OFF_SB + wave * 256, sb_base, (uint32_t)t * 4);
-    else dma4(rws, slot + OFF_SB + wave * 256, sb_base, (uint32_t)t * 4 * nwkb);
   };
-  auto issue_lr = [&](int t) {
-    const uint32_t slot = lds0 + slot_of(t);
-    const int q = t - nst;
-#pragma unroll
-    for (int i = 0; i < 4; i++) dma16(rp, slot + (wave * 64 + 16 * i) * 64, p_base[i], (uint32_t)q * 64);
-#pragma unroll
-    for (int i = 0; i < 2; i++)
-      dma16(rl, slot + OFF_B + (2 * wave + i) * 1024, l_base[i], BWD ? (uint32_t)q * 32 : (uint32_t)q * 16 * N * 2);
+  // Low-rank stage u (chunk q = u - nst), part 1, load v < 8: rows wave*64 +
+  // 8v + [0,8) of the P chunk [256 rows][32 fp32], laid out like the A tile.
+  auto lr_part1_one = [&](int u, int v, bool hf) {
+    const uint32_t slot = lds0 + slot_of(u);
+    const int q = u - nst;
+    const int r = m0 + wave * 64 + 8 * v + r8;
+    const uint32_t off = (r < M && !(hf && upper)) ? (uint32_t)r * R * 4 + (c8 ^ (v & 1)) * 16 : kOobOffset;
+    dma16(rp, slot + (wave * 64 + 8 * v) * 128, off, (uint32_t)q * 128);
   };
-  auto issue = [&](int t) {
-    if (t >= total) return;
-    if (t < nst) issue_fp4(t);
-    else issue_lr(t);
-  };
-
-  // Loads one wave issues for stage u (0 past the end).
-  auto loads_of = [&](int u) { return u >= total ? 0 : (u < nst ? LOADS_FP4 : LOADS_LR); };
-  // Wait until at most n of this wave's loads are outstanding, then barrier:
-  // with n = the loads issued after stage u, stage u is in LDS for every wave.
-  auto publish = [&](int n) {
-    switch (n) {
-      case 0: wait_vm<0>(); break;
-      case LOADS_LR: wait_vm<LOADS_LR>(); break;
-      case LOADS_FP4: wait_vm<LOADS_FP4>(); break;
-      case 2 * LOADS_LR: wait_vm<2 * LOADS_LR>(); break;
-      case LOADS_FP4 + LOADS_LR: wait_vm<LOADS_FP4 + LOADS_LR>(); break;
-      default: wait_vm<2 * LOADS_FP4>(); break;
+  // Low-rank stage u, part 2, load v < 4 (instruction ins = 4 wave + v):
+  //   forward U chunk [32 j][256 n] (512-byte rows): rows 2 ins, 2 ins + 1;
+  //     lane L -> row + L/32, chunk (L%32) ^ (2*(row&3));
+  //   backward D chunk [256 k][32 j] (64-byte rows): rows 16 ins + [0,16);
+  //     lane L -> row + L/4, chunk (L%4) ^ swz64(row).
+  auto lr_part2_one = [&](int u, int v, bool hf) {
+    const uint32_t slot = lds0 + slot_of(u);
+    const int q = u - nst;
+    const int ins = 4 * wave + v;
+    if constexpr (!BWD) {
+      // rows 16..31 of a half chunk (waves 2, 3) are past U
+      const int j = 2 * ins + (lane >> 5);
+      const int c = (lane & 31) ^ (2 * (j & 3));
+      const uint32_t off =
+          (n0 + c * 8 < N && !(hf && wave >= 2)) ? (uint32_t)j * N * 2 + (uint32_t)(n0 + c * 8) * 2 : kOobOffset;
+      dma16(rl, slot + OFF_B + ins * 1024, off, (uint32_t)q * 32 * N * 2);
+    } else {
+      // columns 16..31 of a half chunk (logical chunks 2, 3) are past D's rows
+      const int k = 16 * ins + (lane >> 2);
+      const int c = (lane & 3) ^ swz64(k);
+      const uint32_t off = (n0 + k < K && !(hf && (c & 2))) ? (uint32_t)(n0 + k) * R * 2 + c * 16 : kOobOffset;
+      dma16(rl, slot + OFF_B + ins * 1024, off, (uint32_t)q * 64);
     }
-    // plain barrier: the LDS data it publishes was written by buffer loads,
-    // whose completion the vmcnt wait above already covers
+  };
+  auto issue_part1 = [&](int u) {
+    if (u >= total) return;
+    if (u < nst) {
+      const bool hf = half_last && u == nst - 1;
+#pragma unroll
+      for (int v = 0; v < 10; v++) fp4_part1_one(u, v, hf);
+    } else {
+      const bool hf = half_lr && u == total - 1;
+#pragma unroll
+      for (int v = 0; v < 8; v++) lr_part1_one(u, v, hf);
+    }
+  };
+  auto issue_part2 = [&](int u) {
+    if (u >= total) return;
+    if (u < nst) {
+      const bool hf = half_last && u == nst - 1;
+#pragma unroll
+      for (int v = 0; v < 9; v++) fp4_part2_one(u, v, hf);
+    } else {
+      const bool hf = half_lr && u == total - 1;
+#pragma unroll
+      for (int v = 0; v < 4; v++) lr_part2_one(u, v, hf);
+    }
+  };
+  // Loads of either part for a stage of any kind, as one fixed instruction
+  // sequence whose operands are picked by the (uniform) kind: the tail of the
+  // tile runs without branches between its MFMAs.  A load a kind does not
+  // have reads zeros (kOobOffset) into a part of the slot that kind leaves
+  // unused; a stage past the end reads zeros into its free slot.  The
+  // choices are made once per stage (bitwise logic: no branches).
+  constexpr uint32_t SPARE = 48 * 1024;   // unused by low-rank stages: 4 waves x 1 KB
+  struct StageSel { uint32_t slot; int u, q; bool fp, lr, hf; };
+  auto stage_sel = [&](int u) {
+    StageSel t;
+    const int k = kind_of(u);
+    t.u = u;
+    t.q = u - nst;
+    t.slot = lds0 + slot_of(u);
+    t.fp = k == SK_FP4;
+    t.lr = k == SK_LR;
+    t.hf = t.lr ? (half_lr & (u == total - 1)) : (half_last & (u == nst - 1));
+    return t;
+  };
+  auto any_part1_one = [&](const StageSel& t, int v) {
+    if (v < 8) {
+      const int r = m0 + wave * 64 + 8 * v + r8;
+      const uint32_t p_off = (r < M) ? (uint32_t)r * R * 4 + (c8 ^ (v & 1)) * 16 : kOobOffset;
+      const bool zero = !(t.fp | t.lr) | (t.hf & upper);
+      const uint32_t off = zero ? kOobOffset : (t.lr ? p_off : a_base[v]);
+      dma16(t.lr ? rp : ra, t.slot + (wave * 64 + 8 * v) * 128, off,
+            t.lr ? (uint32_t)t.q * 128 : (uint32_t)t.u * PROW);
+    } else {
+      const bool zero = !t.fp | (t.hf & ((lane & 1) != 0));
+      dma4(ras, t.slot + OFF_SA + (wave * 64 + 32 * (v - 8)) * 8, zero ? kOobOffset : sa_base[v - 8],
+           (uint32_t)t.u * 8);
+    }
+  };
+  auto any_part2_one = [&](const StageSel& t, int v) {
+    // zero halves of a half stage: forward W upper chunks; backward W rows of waves 2, 3
+    const bool w_cut = BWD ? (t.hf & (wave >= 2)) : (t.hf & upper);
+    if (v < 8) {
+      const uint32_t w_off = (t.fp & !w_cut) ? w_base[v] : kOobOffset;
+      const uint32_t w_dst = t.slot + OFF_B + (wave * 64 + 8 * v) * PROW;
+      const uint32_t w_so = BWD ? (uint32_t)t.u * PK * ldw : (uint32_t)t.u * PROW;
+      if (v < 4) {
+        const int ins = 4 * wave + v;
+        uint32_t l_off, l_so;
+        if constexpr (!BWD) {
+          // rows 16..31 of a half chunk (waves 2, 3) are past U
+          const int j = 2 * ins + (lane >> 5);
+          const int c = (lane & 31) ^ (2 * (j & 3));
+          const bool ok = (n0 + c * 8 < N) & !(t.hf & (wave >= 2));
+          l_off = ok ? (uint32_t)j * N * 2 + (uint32_t)(n0 + c * 8) * 2 : kOobOffset;
+          l_so = (uint32_t)t.q * 32 * N * 2;
+        } else {
+          // columns 16..31 of a half chunk (logical chunks 2, 3) are past D's rows
+          const int kk = 16 * ins + (lane >> 2);
+          const int c = (lane & 3) ^ swz64(kk);
+          const bool ok = (n0 + kk < K) & !(t.hf & ((c & 2) != 0));
+          l_off = ok ? (uint32_t)(n0 + kk) * R * 2 + c * 16 : kOobOffset;
+          l_so = (uint32_t)t.q * 64;
+        }
+        dma16(t.lr ? rl : rw, t.lr ? t.slot + OFF_B + ins * 1024 : w_dst, t.lr ? l_off : w_off,
+              t.lr ? l_so : w_so);
+      } else {
+        dma16(rw, t.lr ? t.slot + SPARE + wave * 1024 : w_dst, w_off, w_so);
+      }
+    } else {
+      const bool s_cut = BWD ? (t.hf & (wave >= 2)) : (t.hf & ((lane & 1) != 0));
+      dma4(rws, t.slot + OFF_SB + wave * 256, (t.fp & !s_cut) ? sb_base : kOobOffset,
+           BWD ? (uint32_t)t.u * 8 * nwkb : (uint32_t)t.u * 8);
+    }
+  };
+  // Loads of part 1 of stage u (the count a wait leaves outstanding).
+  auto part1_loads = [&](int u) { return u >= total ? 0 : (u < nst ? LOADS_A : LOADS_P); };
+  // Every load this wave issued has landed and its own LDS reads are done;
+  // after the barrier the same holds for all waves.
+  auto publish_all = [&]() {
+    __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");     // no LDS read moves above the barrier
+    asm volatile("" ::: "memory");        // no LDS read moves above the barrier
   };
 
   // ---------------- fragment reads
-  const int sw_a = swz64(r32);                      // rows ... + r32 of 64-byte-row tiles
-  const int sw_t = (t16 & 7) ^ ((t16 >> 3) & 1);    // rows ... + t16 of the backward W tile
-  const uint32_t psel = h ? 0x0301u : 0x0200u;      // result bytes 0,1 = scale bytes h, h+2 of a dword
+  const int sw_r = swz128(r32);                     // rows ... + r32 of 128-byte-row tiles
+  const int sw_t = swz128(t16);                     // rows ... + t16 of the backward W tile
+  const int sw_d = swz64(r32);                      // rows ... + r32 of the backward D chunk
+  const uint32_t psel = h ? 0x07050301u : 0x06040200u;   // bytes h, h+2, h+4, h+6 of a dword pair
 
-  // Per-lane LDS read offsets within a slot, one set per k-step (a fragment
-  // read is then one address add plus an immediate offset).
-  uint32_t rd_a[2], rd_b[2], rd_t[2][4];
+  // Per-lane LDS read offsets within a slot, one per k-step (a fragment read
+  // is then one address add plus an immediate offset).
+  uint32_t rd_a[4], rd_b[4], rd_t[4];
 #pragma unroll
-  for (int kk = 0; kk < 2; kk++) {
-    rd_a[kk] = (wm * 128 + r32) * PROW + (((2 * kk + h) ^ sw_a) << 4);
-    rd_b[kk] = OFF_B + (wn * 128 + r32) * PROW + (((2 * kk + h) ^ sw_a) << 4);
-#pragma unroll
-    for (int j = 0; j < 4; j++)
-      rd_t[kk][j] = OFF_B + (kk * 64 + 32 * h + t16) * 128 + (((wn * 4 + j) ^ sw_t) << 4) + 8 * (g16 & 1);
+  for (int kk = 0; kk < 4; kk++) {
+    rd_a[kk] = (wm * 128 + r32) * PROW + (((2 * kk + h) ^ sw_r) << 4);
+    rd_b[kk] = OFF_B + (wn * 128 + r32) * PROW + (((2 * kk + h) ^ sw_r) << 4);
   }
-  const uint32_t rd_sa = OFF_SA + (wm * 128 + r32) * 4;
-  const uint32_t rd_sbt = OFF_SB + h * 256 + wn * 4;     // backward W-scale rows h (+2)
+#pragma unroll
+  for (int j = 0; j < 4; j++)   // + kk * 64 rows for k-step kk
+    rd_t[j] = OFF_B + (32 * h + t16) * 128 + (((wn * 4 + j) ^ sw_t) << 4) + 8 * (g16 & 1);
+  const uint32_t rd_sa = OFF_SA + (wm * 128 + r32) * 8;
 
   struct Fp4Frag { v4i a[4], b[4]; };
-  auto read_fp4 = [&](int t, int kk, Fp4Frag& f) {
-    const uint8_t* slot = lds + slot_of(t);
-    const uint8_t* pa = slot + rd_a[kk];
-#pragma unroll
-    for (int i = 0; i < 4; i++) f.a[i] = *(const v4i*)(pa + i * 32 * PROW);
-    if constexpr (!BWD) {
-      const uint8_t* pb = slot + rd_b[kk];
-#pragma unroll
-      for (int j = 0; j < 4; j++) f.b[j] = *(const v4i*)(pb + j * 32 * PROW);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; j++) {
-        const uint8_t* pt = slot + rd_t[kk][j];
-        const v2i lo = lds_read_tr4((const FT_LDS void*)pt);
-        const v2i hi = lds_read_tr4((const FT_LDS void*)(pt + 16 * 128));
-        f.b[j] = v4i{lo[0], lo[1], hi[0], hi[1]};
-      }
-    }
-  };
-  // Single-fragment reads, for interleaving with the MFMAs one at a time.
-  // Fragment q of a k-step: q < 4 -> A row tile q; q >= 4 -> W tile q - 4
+  // Fragment q of k-step kk: q < 4 -> A row tile q; q >= 4 -> W tile q - 4
   // (backward: its two transposing halves are fragments 4 + 2j and 5 + 2j).
   constexpr int FRAG_READS = BWD ? 12 : 8;
   auto read_one = [&](int t, int kk, int q, Fp4Frag& f) {
@@ -487,111 +591,105 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       f.b[q - 4] = *(const v4i*)(slot + rd_b[kk] + (q - 4) * 32 * PROW);
     } else {
       const int j = (q - 4) >> 1, half = (q - 4) & 1;
-      const v2i v = lds_read_tr4((const FT_LDS void*)(slot + rd_t[kk][j] + half * 16 * 128));
+      const v2i v = lds_read_tr4((const FT_LDS void*)(slot + rd_t[j] + (kk * 64 + half * 16) * 128));
       if (half == 0) { f.b[j][0] = v[0]; f.b[j][1] = v[1]; }
       else { f.b[j][2] = v[0]; f.b[j][3] = v[1]; }
     }
   };
-  // Raw scale words of a stage; turned into MFMA scale operands (one byte per
-  // k-step) only when the stage's MFMAs are about to issue.
-  struct ScaleRaw { uint32_t a[4], b[4]; };
-  auto read_scales = [&](int t, ScaleRaw& r) {
-    const uint8_t* slot = lds + slot_of(t);
+  // Raw scale words of a stage (8 blocks per row or column block); turned
+  // into MFMA scale operands (one byte per k-step) only when the stage's
+  // MFMAs are about to issue.
+  struct ScaleRaw { uint32_t a[8], b[8]; };
+  auto read_scales_a = [&](const uint8_t* slot, ScaleRaw& r) {
 #pragma unroll
-    for (int i = 0; i < 4; i++) r.a[i] = *(const uint32_t*)(slot + rd_sa + i * 128);
+    for (int i = 0; i < 4; i++) {
+      const v2i d = *(const v2i*)(slot + rd_sa + i * 256);
+      r.a[2 * i] = (uint32_t)d[0];
+      r.a[2 * i + 1] = (uint32_t)d[1];
+    }
+  };
+  auto read_scales_b = [&](const uint8_t* slot, ScaleRaw& r) {
     if constexpr (!BWD) {
 #pragma unroll
-      for (int j = 0; j < 4; j++) {  // 32-column block wn*4 + j, staged by wave (wn*4+j)/2
-        r.b[j] = *(const uint32_t*)(slot + OFF_SB + (wn * 2 + (j >> 1)) * 256 + (j & 1) * 4);
+      for (int j = 0; j < 4; j++) {   // 32-column block b = wn*4 + j
+        const int b = wn * 4 + j;
+        const v2i d = *(const v2i*)(slot + OFF_SB + (b >> 1) * 256 + (b & 1) * 8);
+        r.b[2 * j] = (uint32_t)d[0];
+        r.b[2 * j + 1] = (uint32_t)d[1];
       }
     } else {
-      // rows 2kk + h of this stage's W-scale block (staged by wave 2kk+h), column blocks wn*4 + j
-      r.b[0] = *(const uint32_t*)(slot + rd_sbt);
-      r.b[1] = *(const uint32_t*)(slot + rd_sbt + 512);
+#pragma unroll
+      for (int kk = 0; kk < 4; kk++)   // reduction block 2kk + h, column blocks wn*4 .. +3
+        r.b[kk] = *(const uint32_t*)(slot + OFF_SB + kk * 256 + h * 8 + wn * 4);
     }
   };
   auto scale_ops = [&](const ScaleRaw& r, uint32_t (&sa)[4], uint32_t (&sb)[4]) {
 #pragma unroll
-    for (int i = 0; i < 4; i++) sa[i] = __builtin_amdgcn_perm(0u, r.a[i], psel);
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-      if constexpr (!BWD) sb[j] = __builtin_amdgcn_perm(0u, r.b[j], psel);
-      else sb[j] = __builtin_amdgcn_perm(r.b[1], r.b[0], 0x0c0c0400u | (j << 8) | j);
-    }
-  };
-
-  struct LrFrag { v4i p[4][2]; v8bf b[4]; };
-  const int jj = t16 >> 2, qq = t16 & 3;
-  auto read_lr = [&](int t, LrFrag& f) {
-    const uint8_t* slot = lds + slot_of(t);
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const uint8_t* row = slot + (wm * 128 + i * 32 + r32) * 64;
-      f.p[i][0] = *(const v4i*)(row + (((2 * h) ^ sw_a) << 4));
-      f.p[i][1] = *(const v4i*)(row + (((2 * h + 1) ^ sw_a) << 4));
-    }
+    for (int i = 0; i < 4; i++) sa[i] = __builtin_amdgcn_perm(r.a[2 * i + 1], r.a[2 * i], psel);
 #pragma unroll
     for (int j = 0; j < 4; j++) {
       if constexpr (!BWD) {
-        const int n = wn * 128 + j * 32 + 16 * (g16 & 1) + 4 * qq;
-        const int row0 = 8 * h + jj;
-        const int byte0 = ((((n >> 3) ^ (2 * (row0 & 3))) << 4)) + ((n >> 2) & 1) * 8;
-        const v4s lo = lds_read_tr16((const FT_LDS void*)(slot + OFF_B + row0 * 512 + byte0));
-        const int row1 = row0 + 4;
-        const int byte1 = ((((n >> 3) ^ (2 * (row1 & 3))) << 4)) + ((n >> 2) & 1) * 8;
-        const v4s hi = lds_read_tr16((const FT_LDS void*)(slot + OFF_B + row1 * 512 + byte1));
-        f.b[j] = make_v8bf(lo, hi);
+        sb[j] = __builtin_amdgcn_perm(r.b[2 * j + 1], r.b[2 * j], psel);
       } else {
-        const int k = wn * 128 + j * 32 + r32;
-        f.b[j] = __builtin_bit_cast(v8bf, *(const v4i*)(slot + OFF_B + k * 32 + ((h ^ ((k >> 2) & 1)) << 4)));
+        sb[j] = __builtin_amdgcn_perm(r.b[1], r.b[0], 0x0c0c0400u | (j << 8) | j) |
+                __builtin_amdgcn_perm(r.b[3], r.b[2], 0x04000c0cu | (j << 24) | (j << 16));
       }
     }
   };
 
   v16f acc[4][4];
 
-  auto mfma_fp4_step = [&](int kk, const Fp4Frag& f, const uint32_t (&sa)[4], const uint32_t (&sb)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; i++)
-#pragma unroll
-      for (int j = 0; j < 4; j++) {
-        if (kk == 0) acc[i][j] = mfma_fp4_32x32x64<0>(f.b[j], f.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
-        else acc[i][j] = mfma_fp4_32x32x64<1>(f.b[j], f.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
-      }
-  };
-  auto mfma_lr_step = [&](const LrFrag& f) {
-    v8bf ahi[4], alo[4];
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const v4i x0 = f.p[i][0], x1 = f.p[i][1];
-      const int xs[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-      v4i hh, ll;
-#pragma unroll
-      for (int e = 0; e < 4; e++) {
-        uint32_t hp, lp;
-        split_bf16x2(__int_as_float(xs[2 * e]), __int_as_float(xs[2 * e + 1]), hp, lp);
-        hh[e] = (int)hp;
-        ll[e] = (int)lp;
-      }
-      ahi[i] = __builtin_bit_cast(v8bf, hh);
-      alo[i] = __builtin_bit_cast(v8bf, ll);
+  // Low-rank fragments, one 16-column half c of a stage at a time: the raw
+  // LDS words (P fp32, U or D bf16), and the MFMA operands made from them
+  // (each P pair split into bf16 hi + lo).
+  struct LrRaw { v4i p[4][2]; v4i b[4]; };
+  struct LrOps { v4i hi[4], lo[4]; };
+  const int jj = t16 >> 2, qq = t16 & 3;
+  // Read q of half c of low-rank stage t: q < 8 -> P row tile q/2, dwords
+  // 4(q%2)..+3 of the lane's eight; then the U / D fragment of each column
+  // tile (forward: two transposing reads of 4 rows each).
+  constexpr int LR_READS = BWD ? 12 : 16;
+  auto lr_read_one = [&](int t, int c, int q, LrRaw& f) {
+    const uint8_t* slot = lds + slot_of(t);
+    if (q < 8) {
+      const int i = q >> 1, e = q & 1;
+      f.p[i][e] = *(const v4i*)(slot + (wm * 128 + i * 32 + r32) * 128 + (((4 * c + 2 * h + e) ^ sw_r) << 4));
+    } else if constexpr (!BWD) {
+      const int j = (q - 8) >> 1, half = (q - 8) & 1;
+      const int n = wn * 128 + j * 32 + 16 * (g16 & 1) + 4 * qq;
+      const int row = 16 * c + 8 * h + jj + 4 * half;
+      const int byte = ((((n >> 3) ^ (2 * (row & 3))) << 4)) + ((n >> 2) & 1) * 8;
+      const v2i v = __builtin_bit_cast(v2i, lds_read_tr16((const FT_LDS void*)(slot + OFF_B + row * 512 + byte)));
+      f.b[j][2 * half] = v[0];
+      f.b[j][2 * half + 1] = v[1];
+    } else {
+      const int j = q - 8;
+      const int k = wn * 128 + j * 32 + r32;
+      f.b[j] = *(const v4i*)(slot + OFF_B + k * 64 + (((2 * c + h) ^ sw_d) << 4));
     }
-#pragma unroll
-    for (int i = 0; i < 4; i++)
-#pragma unroll
-      for (int j = 0; j < 4; j++) {
-        acc[i][j] = mfma_bf16_32x32x16(f.b[j], ahi[i], acc[i][j]);
-        acc[i][j] = mfma_bf16_32x32x16(f.b[j], alo[i], acc[i][j]);
-      }
+  };
+  // Split pair e (fp32 elements 2e, 2e+1) of row tile i into bf16 hi + lo.
+  auto lr_split = [&](const LrRaw& f, int i, int e, LrOps& o) {
+    const v4i x = f.p[i][e >> 1];
+    uint32_t hp, lp;
+    split_bf16x2(__int_as_float(x[2 * (e & 1)]), __int_as_float(x[2 * (e & 1) + 1]), hp, lp);
+    o.hi[i][e] = (int)hp;
+    o.lo[i][e] = (int)lp;
+  };
+  // MFMA m of a low-rank half: m < 16 -> hi terms of tile (m/4, m%4), then the
+  // lo terms in the same order (no accumulator is used twice in a row).
+  auto lr_mfma = [&](int m, const LrRaw& f, const LrOps& o) {
+    const int i = (m >> 2) & 3, j = m & 3;
+    const v4i a = m < 16 ? o.hi[i] : o.lo[i];
+    acc[i][j] = mfma_bf16_32x32x16(__builtin_bit_cast(v8bf, f.b[j]), __builtin_bit_cast(v8bf, a), acc[i][j]);
   };
 
   // ---------------- pipeline
-  // Stage t's slot is refilled (with stage t+4) in iteration t+1, after that
-  // iteration's barrier; every wave passed its own wait for the reads of slot t
-  // (the wait at the top of iteration t+1) before arriving there.
-  issue(0);
-  issue(1);
-  issue(2);
+  // Stage u: part 1 issued in iteration u-2 (after its barrier), part 2 in
+  // iteration u-1 (first k-step); stages 0 and 1 start here.
+  issue_part1(0);
+  issue_part2(0);
+  issue_part1(1);
   // Accumulators start at the bias (forward): every output's sum begins with
   // its bias term, in both output precisions.
 #pragma unroll
@@ -605,75 +703,78 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         acc[i][j][4 * q + 2] = bf16_to_f32(bias4[j][q].y & 0xFFFFu);
         acc[i][j][4 * q + 3] = bf16_to_f32(bias4[j][q].y >> 16);
       }
-  publish(loads_of(1) + loads_of(2));
+  switch (part1_loads(1)) {   // stage 0 landed; part 1 of stage 1 may stay in flight
+    case LOADS_A: wait_vm<LOADS_A>(); break;
+    case LOADS_P: wait_vm<LOADS_P>(); break;
+    default: wait_vm<0>(); break;
+  }
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
   Fp4Frag f0, f1;
   ScaleRaw sr;
-  read_fp4(0, 0, f0);
-  read_scales(0, sr);
-
-  // One FP4 iteration.  STEADY: stages t+1..t+3 are FP4 stages, so the body is
-  // branch-free with constant wait counts, and every other instruction is
-  // placed between two MFMAs (one wave per SIMD: the matrix pipe only stays
-  // busy if nothing else waits in front of the next MFMA):
-  //   k-step 0 (16 MFMAs on f0) carries the reads of this stage's k-step 1;
-  //   then the barrier that publishes stage t+1;
-  //   k-step 1 (16 MFMAs on f1) carries the reads of stage t+1's k-step 0 and
-  //   scales, the loads of stage t+3, and the scale operands of stage t+1.
   uint32_t sa[4], sb[4];
+  LrRaw ga, gb;   // the two halves of a low-rank stage
+#pragma unroll
+  for (int q = 0; q < FRAG_READS; q++) read_one(0, 0, q, f0);
+  read_scales_a(lds + slot_of(0), sr);
+  read_scales_b(lds + slot_of(0), sr);
   scale_ops(sr, sa, sb);
-  auto fp4_iter_steady = [&](int t) {
-    const uint8_t* nslot = lds + slot_of(t + 1);
-    const uint32_t dslot = lds0 + slot_of(t + 3);
-    const uint32_t a_off = (uint32_t)(t + 3) * PROW;
-    const uint32_t wt_off = (uint32_t)(t + 3) * PK * ldw;
-    const uint32_t s_off = (uint32_t)(t + 3) * 4;
+
+  // One FP4 iteration.  ANY = 0: stages s+1 and s+2 are whole FP4 stages;
+  // ANY = 1: they may be of any kind (their loads pick operands by kind, and
+  // the reads of stage s+1 as FP4 fragments are simply unused when it is
+  // not).  Every other instruction sits between two MFMAs (one wave per SIMD:
+  // the matrix pipe only stays busy if nothing waits in front of the next
+  // MFMA):
+  //   k-step 0 carries the reads of k-step 1 and part 2 of stage s+1;
+  //   k-steps 1, 2 carry the reads of k-steps 2, 3;
+  //   the barrier publishes stage s+1 and frees the slot of stage s;
+  //   k-step 3 carries the reads of stage s+1's k-step 0 and scales, part 1
+  //   of stage s+2, and the scale operands of stage s+1.
+  auto fp4_body = [&](int s, auto anyc) {
+    constexpr bool ANY = decltype(anyc)::value != 0;
+    const StageSel t2 = stage_sel(s + 1), t1 = stage_sel(s + 2);
+    const uint8_t* nslot = lds + slot_of(s + 1);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int m = 0; m < 16; m++) {
       const int i = m >> 2, j = m & 3;
       acc[i][j] = mfma_fp4_32x32x64<0>(f0.b[j], f0.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
-      if (m < FRAG_READS) read_one(t, 1, m, f1);
+      if (m < FRAG_READS) read_one(s, 1, m, f1);
+      if (m < 9) {
+        if constexpr (ANY) any_part2_one(t2, m);
+        else fp4_part2_one(s + 1, m, false);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
-    wait_vm<LOADS_FP4>();                // stage t+1 landed; stage t+2 may stay in flight
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int m = 0; m < 16; m++) {
+      const int i = m >> 2, j = m & 3;
+      acc[i][j] = mfma_fp4_32x32x64<1>(f1.b[j], f1.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
+      if (m < FRAG_READS) read_one(s, 2, m, f0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int m = 0; m < 16; m++) {
+      const int i = m >> 2, j = m & 3;
+      acc[i][j] = mfma_fp4_32x32x64<2>(f0.b[j], f0.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
+      if (m < FRAG_READS) read_one(s, 3, m, f1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    publish_all();
     __builtin_amdgcn_sched_barrier(0);
     uint32_t nsa[4], nsb[4];
 #pragma unroll
     for (int m = 0; m < 16; m++) {
       const int i = m >> 2, j = m & 3;
-      acc[i][j] = mfma_fp4_32x32x64<1>(f1.b[j], f1.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
-      // reads of stage t+1: fragments in slots 0..FRAG_READS-1, then scales
-      if (m < FRAG_READS) read_one(t + 1, 0, m, f0);
-      if (m == FRAG_READS - 4 || (BWD && m == 12)) {
-        if (m == FRAG_READS - 4) {
-#pragma unroll
-          for (int q = 0; q < 4; q++) sr.a[q] = *(const uint32_t*)(nslot + rd_sa + q * 128);
-        }
-        if (!BWD || m == 12) {
-          if constexpr (!BWD) {
-#pragma unroll
-            for (int q = 0; q < 4; q++)
-              sr.b[q] = *(const uint32_t*)(nslot + OFF_SB + (wn * 2 + (q >> 1)) * 256 + (q & 1) * 4);
-          } else {
-            sr.b[0] = *(const uint32_t*)(nslot + rd_sbt);
-            sr.b[1] = *(const uint32_t*)(nslot + rd_sbt + 512);
-          }
-        }
+      acc[i][j] = mfma_fp4_32x32x64<3>(f1.b[j], f1.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
+      if (m < FRAG_READS) read_one(s + 1, 0, m, f0);
+      if (m == FRAG_READS - 4) read_scales_a(nslot, sr);
+      if (m == FRAG_READS - 2) read_scales_b(nslot, sr);
+      if (m < 10) {
+        if constexpr (ANY) any_part1_one(t1, m);
+        else fp4_part1_one(s + 2, m, false);
       }
-      // loads of stage t+3: A tile rows in slots 0..3, W tile in 4..7, scales in 8, 9
-      if (m < 4) dma16(ra, dslot + (wave * 64 + 16 * m) * PROW, a_base[m], a_off);
-      else if (m < 8) {
-        if constexpr (!BWD) dma16(rw, dslot + OFF_B + (wave * 64 + 16 * (m - 4)) * PROW, w_base[m - 4], a_off);
-        else dma16(rw, dslot + OFF_B + (wave * 32 + 8 * (m - 4)) * 128, wt_base[m - 4], wt_off);
-      } else if (m == 8) {
-        dma4(ras, dslot + OFF_SA + wave * 256, sa_base, s_off);
-      } else if (m == 9) {
-        if constexpr (!BWD) dma4(rws, dslot + OFF_SB + wave * 256, sb_base, s_off);
-        else dma4(rws, dslot + OFF_SB + wave * 256, sb_base, s_off * nwkb);
-      }
-      // scale operands of stage t+1 once its scale words are in registers
       if (m == 15) scale_ops(sr, nsa, nsb);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -681,44 +782,53 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     for (int q = 0; q < 4; q++) { sa[q] = nsa[q]; sb[q] = nsb[q]; }
   };
 
-  // Remaining FP4 iterations (the last three stages): loads may run out, so
-  // waits and issues follow the stage kinds.
-  auto fp4_iter = [&](int t) {
-    read_fp4(t, 1, f1);
+  // One low-rank iteration (stage s >= nst, its first half in ga):
+  //   half 0: 32 MFMAs carrying the hi/lo splits of its row tiles 1..3, the
+  //   reads of half 1 and part 2 of stage s+1;
+  //   the barrier publishes stage s+1 and frees the slot of stage s;
+  //   half 1: likewise, carrying part 1 of stage s+2 and the reads of stage
+  //   s+1's first half (unused past the last stage).
+  // The second half of a 16-column last stage reads as zeros and adds zeros.
+  auto lr_body = [&](int s) {
+    const StageSel t2 = stage_sel(s + 1), t1 = stage_sel(s + 2);
+    LrOps o;
+#pragma unroll
+    for (int e = 0; e < 4; e++) lr_split(ga, 0, e, o);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_fp4_step(0, f0, sa, sb);
-    __builtin_amdgcn_sched_barrier(0);
-    publish(loads_of(t + 2));
-    issue(t + 3);
-    if (t + 1 < nst) {
-      read_fp4(t + 1, 0, f0);
-      read_scales(t + 1, sr);
+#pragma unroll
+    for (int m = 0; m < 32; m++) {
+      lr_mfma(m, ga, o);
+      if (m < 12) lr_split(ga, (m >> 2) + 1, m & 3, o);
+      if (m >= 16 && m - 16 < LR_READS) lr_read_one(s, 1, m - 16, gb);
+      if (m < 4) any_part2_one(t2, m);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    publish_all();
     __builtin_amdgcn_sched_barrier(0);
-    mfma_fp4_step(1, f1, sa, sb);
+#pragma unroll
+    for (int e = 0; e < 4; e++) lr_split(gb, 0, e, o);
     __builtin_amdgcn_sched_barrier(0);
-    if (t + 1 < nst) scale_ops(sr, sa, sb);
+#pragma unroll
+    for (int m = 0; m < 32; m++) {
+      lr_mfma(m, gb, o);
+      if (m < 12) lr_split(gb, (m >> 2) + 1, m & 3, o);
+      if (m < 8) any_part1_one(t1, m);
+      if (m >= 16 && m - 16 < LR_READS) lr_read_one(s + 1, 0, m - 16, ga);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
-  int t = 0;
+
+  int s = 0;
+  // stages s+1, s+2 whole FP4 stages: the loop the tile spends most time in
 #pragma unroll 1
-  for (; t + 3 < nst; t++) fp4_iter_steady(t);
+  for (; s + 2 < nfull; s++) fp4_body(s, IC<0>{});
 #pragma unroll 1
-  for (; t < nst; t++) fp4_iter(t);
+  for (; s < nst; s++) fp4_body(s, IC<1>{});
   if (nlr > 0) {
-    LrFrag g;
-    read_lr(nst, g);
+#pragma unroll
+    for (int q = 0; q < LR_READS; q++) lr_read_one(nst, 0, q, ga);
 #pragma unroll 1
-    for (int t = nst; t < total; t++) {
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // this wave's reads of slot t-1 are done
-      publish(loads_of(t + 2));
-      issue(t + 3);
-      LrFrag gn;
-      if (t + 1 < total) read_lr(t + 1, gn);
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_lr_step(g);
-      __builtin_amdgcn_sched_barrier(0);
-      g = gn;
-    }
+    for (; s < total; s++) lr_body(s);
   }
 
   // ---------------- epilogue: convert, store
@@ -946,7 +1056,7 @@ hipError_t launch_gemm_fp4(bool bwd, const uint8_t* a, const uint8_t* as, const 
   // buffer ranges are 32-bit: the pipelined kernel takes operands below 2 GiB
   const bool small = (size_t)M * KR / 2 < (1u << 31) && (size_t)N * K / 2 < (1u << 31) &&
                      (size_t)M * (R > 0 ? R : 1) * 4 < (1u << 31) && (size_t)M * NO * 2 < (1u << 31);
-  if (KR % PK == 0 && K % 128 == 0 && small) {
+  if (KR % 128 == 0 && K % 128 == 0 && small) {
     const unsigned grid = (unsigned)(tm * tn);
     const GemmEpilogue none{};
     if (!bwd) {
@@ -971,7 +1081,7 @@ hipError_t launch_gemm_fp4(bool bwd, const uint8_t* a, const uint8_t* as, const 
 
 static bool pipe_ok(bool bwd, int M, int N, int K, int R) {
   const int NO = bwd ? K : N, KR = bwd ? N : K;
-  return KR % PK == 0 && K % 128 == 0 && (size_t)M * KR / 2 < (1u << 31) && (size_t)N * K / 2 < (1u << 31) &&
+  return KR % 128 == 0 && K % 128 == 0 && (size_t)M * KR / 2 < (1u << 31) && (size_t)N * K / 2 < (1u << 31) &&
          (size_t)M * (R > 0 ? R : 1) * 4 < (1u << 31) && (size_t)M * NO * 2 < (1u << 31);
 }
 

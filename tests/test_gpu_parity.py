@@ -273,6 +273,45 @@ def test_gemm_random_codes():
     assert np.all(np.abs(host(dx) - dxr) <= 1e-5 * Sdx)
 
 
+@pytest.mark.parametrize("M,K,N,R", [(300, 640, 384, 48), (129, 128, 128, 16), (257, 1280, 896, 80),
+                                     (64, 2304, 640, 0), (520, 1408, 1152, 128), (256, 768, 512, 32)])
+def test_gemm_pipelined_shapes(M, K, N, R):
+    """Reduction lengths that are multiples of 128 run the pipelined kernel:
+    stage counts from one to nine, a half last stage (length an odd multiple
+    of 128) in either direction, low-rank widths with a half last chunk, and
+    row counts that leave partial tiles.  Random code bytes and scales, fp32 P;
+    both output precisions against the oracle."""
+    rng = np.random.default_rng(M + K + N + R)
+    xq = rng.integers(0, 256, (M, K // 2)).astype(np.uint8)
+    xs = rng.integers(110, 140, (M, K // 32)).astype(np.uint8)
+    wq = rng.integers(0, 256, (N, K // 2)).astype(np.uint8)
+    ws = rng.integers(110, 140, (N // 32, K // 32)).astype(np.uint8)
+    gq = rng.integers(0, 256, (M, N // 2)).astype(np.uint8)
+    gs = rng.integers(110, 140, (M, N // 32)).astype(np.uint8)
+    bias = gen.f32_to_bf16_bits(rng.standard_normal(N).astype(np.float32))
+    Pt = Ut = Qt = Dt = None
+    P = U = Qp = D = None
+    if R:
+        P = rng.standard_normal((M, R)).astype(np.float32)
+        U = gen.f32_to_bf16_bits(rng.standard_normal((R, N)).astype(np.float32))
+        Qp = rng.standard_normal((M, R)).astype(np.float32)
+        D = gen.f32_to_bf16_bits(rng.standard_normal((K, R)).astype(np.float32))
+        Pt, Ut = torch.from_numpy(P).to(DEV), dev_bf16(U)
+        Qt, Dt = torch.from_numpy(Qp).to(DEV), dev_bf16(D)
+    args = (dev_u8(xq), dev_u8(xs), dev_u8(wq), dev_u8(ws), K)
+    y32 = _lib.ft_linear_fwd(*args, Pt, Ut, dev_bf16(bias), out_dtype=torch.float32)
+    y16 = _lib.ft_linear_fwd(*args, Pt, Ut, dev_bf16(bias), out_dtype=torch.bfloat16)
+    gargs = (dev_u8(gq), dev_u8(gs), dev_u8(wq), dev_u8(ws), K)
+    dx32 = _lib.ft_linear_bwd_input(*gargs, Qt, Dt, out_dtype=torch.float32)
+    dx16 = _lib.ft_linear_bwd_input(*gargs, Qt, Dt, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    f = (lambda a: None if a is None else a.astype(np.float64))
+    yr, S = ref.linear_fwd(xq, xs, wq, ws, K, f(P), U, bias)
+    check_gemm(host(y32), host(y16), yr, S, "forward")
+    dxr, Sdx = ref.linear_bwd_input(gq, gs, wq, ws, K, f(Qp), D)
+    check_gemm(host(dx32), host(dx16), dxr, Sdx, "backward-input")
+
+
 def test_layer_flux_qkv_full_size_sampled():
     """FLUX.1-dev QKV projection at 1024^2 (M=4608, K=3072, N=9216, r = r_s = 32)
     in the launch configuration the benchmark times: quantized operands
