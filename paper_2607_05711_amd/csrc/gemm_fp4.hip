@@ -259,6 +259,11 @@ constexpr int SLOT = 68 * 1024;          // bytes per ring slot
 constexpr int NSLOT = 2;
 constexpr int OFF_B = 32 * 1024;         // W tile / U / D chunk within a slot
 constexpr int OFF_SA = 64 * 1024;        // A scales: 256 rows x 8 bytes
+// With the reduction length a multiple of 512, the A scales of stages 2q and
+// 2q+1 (16 contiguous bytes per row) load together into a ring of their own:
+// one 16-byte load per row touches half the lines of two 8-byte ones.
+constexpr int OFF_SAP = 2 * 68 * 1024;   // after the two slots
+constexpr int SAP_SLOT = 256 * 16;       // bytes per stage pair; a third slot takes loads that do not apply
 constexpr int OFF_SB = 66 * 1024;        // W scales: 4 waves x 256 bytes
 constexpr int LR_COLS = 32;              // up-projection columns per low-rank stage
 // buffer loads per wave in the first part of a stage: FP4 (A tile, A scales), low-rank (P chunk)
@@ -289,14 +294,15 @@ __device__ __forceinline__ void tile_coords(int bid, int tiles_m, int tiles_n, i
   nt = w / gm;
 }
 
-template <bool BWD, bool OUT_F32, int EPI>
+template <bool BWD, bool OUT_F32, int EPI, bool SAP>
 __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restrict__ A, const uint8_t* __restrict__ As,
                                                           const uint8_t* __restrict__ Wq, const uint8_t* __restrict__ Ws,
                                                           int M, int N, int K, const float* __restrict__ P, int R,
                                                           const uint16_t* __restrict__ LR,
                                                           const uint16_t* __restrict__ bias, void* __restrict__ out,
                                                           int tiles_m, int tiles_n, GemmEpilogue ep) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[NSLOT * SLOT];
+  static_assert(OFF_SAP == NSLOT * SLOT, "pair ring follows the slots");
+  __shared__ __attribute__((aligned(16))) uint8_t lds[NSLOT * SLOT + (SAP ? 3 * SAP_SLOT : 0)];
 
   const int NO = BWD ? K : N;
   const int KR = BWD ? N : K;
@@ -372,6 +378,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     const int r = m0 + wave * 64 + 32 * v + (lane >> 1);
     sa_base[v] = (r < M) ? (uint32_t)r * nkb + 4 * (lane & 1) : kOobOffset;
   }
+  // stage pairs: lane L of wave w loads row w*64 + L (16 bytes) into the pair ring
+  const uint32_t sap_base = (m0 + wave * 64 + lane < M) ? (uint32_t)(m0 + wave * 64 + lane) * nkb : kOobOffset;
   // W scales (lanes 0..3 of each wave, two 8-byte rows per wave):
   //   forward: 32-column block 2w + L/2 of the tile, dword L%2 of the stage;
   //   backward: reduction block 2w + L/2 of the stage, dword L%2 (column
@@ -397,13 +405,23 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   // whose missing part reads as zeros.
   // FP4 stage u, part 1: loads v < 8 fill A-tile rows wave*64 + 8v + [0,8);
   // v = 8, 9 stage A-scale rows wave*64 + 32(v-8) + [0,32).
+  // SAP: the scales of stage pair (u, u+1), u even; go = false sends zeros
+  // to the spare slot instead (no branch).
+  auto pair_load = [&](int u, bool go) {
+    dma16(ras, lds0 + OFF_SAP + (go ? ((u >> 1) & 1) : 2) * SAP_SLOT + wave * 1024, go ? sap_base : kOobOffset,
+          (uint32_t)(u >> 1) * 16);
+  };
+  // (SAP: load 8 of an even stage brings the scales of the stage pair.)
   auto fp4_part1_one = [&](int u, int v, bool hf) {
     const uint32_t slot = lds0 + slot_of(u);
-    if (v < 8)
+    if (v < 8) {
       dma16(ra, slot + (wave * 64 + 8 * v) * PROW, (hf && upper) ? kOobOffset : a_base[v], (uint32_t)u * PROW);
-    else
+    } else if constexpr (SAP) {
+      if (v == 8 && (u & 1) == 0) pair_load(u, true);
+    } else {
       dma4(ras, slot + OFF_SA + (wave * 64 + 32 * (v - 8)) * 8, (hf && (lane & 1)) ? kOobOffset : sa_base[v - 8],
            (uint32_t)u * 8);
+    }
   };
   // FP4 stage u, part 2: loads v < 8 fill W-tile rows wave*64 + 8v + [0,8);
   // v = 8 stages this wave's two W-scale rows.
@@ -508,6 +526,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       const uint32_t off = zero ? kOobOffset : (t.lr ? p_off : a_base[v]);
       dma16(t.lr ? rp : ra, t.slot + (wave * 64 + 8 * v) * 128, off,
             t.lr ? (uint32_t)t.q * 128 : (uint32_t)t.u * PROW);
+    } else if constexpr (SAP) {
+      if (v == 8) pair_load(t.u, t.fp & ((t.u & 1) == 0));
     } else {
       const bool zero = !t.fp | (t.hf & ((lane & 1) != 0));
       dma4(ras, t.slot + OFF_SA + (wave * 64 + 32 * (v - 8)) * 8, zero ? kOobOffset : sa_base[v - 8],
@@ -551,7 +571,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     }
   };
   // Loads of part 1 of stage u (the count a wait leaves outstanding).
-  auto part1_loads = [&](int u) { return u >= total ? 0 : (u < nst ? LOADS_A : LOADS_P); };
+  auto part1_loads = [&](int u) {
+    return u >= total ? 0 : (u < nst ? ((SAP && (u & 1)) ? LOADS_A - 2 : LOADS_A) : LOADS_P);
+  };
   // Every load this wave issued has landed and its own LDS reads are done;
   // after the barrier the same holds for all waves.
   auto publish_all = [&]() {
@@ -600,10 +622,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   // into MFMA scale operands (one byte per k-step) only when the stage's
   // MFMAs are about to issue.
   struct ScaleRaw { uint32_t a[8], b[8]; };
-  auto read_scales_a = [&](const uint8_t* slot, ScaleRaw& r) {
+  auto read_scales_a = [&](int t, ScaleRaw& r) {
+    const uint8_t* base = SAP ? lds + OFF_SAP + ((t >> 1) & 1) * SAP_SLOT + (wm * 128 + r32) * 16 + (t & 1) * 8
+                              : lds + slot_of(t) + rd_sa;
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-      const v2i d = *(const v2i*)(slot + rd_sa + i * 256);
+      const v2i d = *(const v2i*)(base + i * (SAP ? 512 : 256));
       r.a[2 * i] = (uint32_t)d[0];
       r.a[2 * i + 1] = (uint32_t)d[1];
     }
@@ -716,7 +740,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   LrRaw ga, gb;   // the two halves of a low-rank stage
 #pragma unroll
   for (int q = 0; q < FRAG_READS; q++) read_one(0, 0, q, f0);
-  read_scales_a(lds + slot_of(0), sr);
+  read_scales_a(0, sr);
   read_scales_b(lds + slot_of(0), sr);
   scale_ops(sr, sa, sb);
 
@@ -731,8 +755,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   //   the barrier publishes stage s+1 and frees the slot of stage s;
   //   k-step 3 carries the reads of stage s+1's k-step 0 and scales, part 1
   //   of stage s+2, and the scale operands of stage s+1.
-  auto fp4_body = [&](int s, auto anyc) {
+  // PAR (whole stages only): the parity of s, which decides whether k-step 3
+  // loads a pair of A-scale stages (SAP).
+  auto fp4_body = [&](int s, auto anyc, auto parc) {
     constexpr bool ANY = decltype(anyc)::value != 0;
+    constexpr int PAR = decltype(parc)::value;
     const StageSel t2 = stage_sel(s + 1), t1 = stage_sel(s + 2);
     const uint8_t* nslot = lds + slot_of(s + 1);
     __builtin_amdgcn_sched_barrier(0);
@@ -769,11 +796,17 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       const int i = m >> 2, j = m & 3;
       acc[i][j] = mfma_fp4_32x32x64<3>(f1.b[j], f1.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
       if (m < FRAG_READS) read_one(s + 1, 0, m, f0);
-      if (m == FRAG_READS - 4) read_scales_a(nslot, sr);
+      if (m == FRAG_READS - 4) read_scales_a(s + 1, sr);
       if (m == FRAG_READS - 2) read_scales_b(nslot, sr);
       if (m < 10) {
-        if constexpr (ANY) any_part1_one(t1, m);
-        else fp4_part1_one(s + 2, m, false);
+        if constexpr (ANY) {
+          any_part1_one(t1, m);
+        } else if constexpr (SAP) {
+          if (m < 8) fp4_part1_one(s + 2, m, false);
+          else if (m == 8 && PAR == 0) pair_load(s + 2, true);
+        } else {
+          fp4_part1_one(s + 2, m, false);
+        }
       }
       if (m == 15) scale_ops(sr, nsa, nsb);
       __builtin_amdgcn_sched_barrier(0);
@@ -820,10 +853,15 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
 
   int s = 0;
   // stages s+1, s+2 whole FP4 stages: the loop the tile spends most time in
+  // (two stages per trip: the parity of s is known in each body)
 #pragma unroll 1
-  for (; s + 2 < nfull; s++) fp4_body(s, IC<0>{});
+  for (; s + 3 < nfull; s += 2) {
+    fp4_body(s, IC<0>{}, IC<0>{});
+    fp4_body(s + 1, IC<0>{}, IC<1>{});
+  }
+  if (s + 2 < nfull) fp4_body(s++, IC<0>{}, IC<0>{});
 #pragma unroll 1
-  for (; s < nst; s++) fp4_body(s, IC<1>{});
+  for (; s < nst; s++) fp4_body(s, IC<1>{}, IC<0>{});
   if (nlr > 0) {
 #pragma unroll
     for (int q = 0; q < LR_READS; q++) lr_read_one(nst, 0, q, ga);
@@ -1059,13 +1097,18 @@ hipError_t launch_gemm_fp4(bool bwd, const uint8_t* a, const uint8_t* as, const 
   if (KR % 128 == 0 && K % 128 == 0 && small) {
     const unsigned grid = (unsigned)(tm * tn);
     const GemmEpilogue none{};
-    if (!bwd) {
-      if (out_f32) k_gemm_fp4_pipe<false, true, EPI_PLAIN><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out, tm, tn, none);
-      else k_gemm_fp4_pipe<false, false, EPI_PLAIN><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, out, tm, tn, none);
+    const uint16_t* b = bwd ? nullptr : bias;
+    // A scales in stage pairs when the reduction length is a multiple of 512
+#define FT_PIPE(BW, F32, SP) \
+  k_gemm_fp4_pipe<BW, F32, EPI_PLAIN, SP><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, b, out, tm, tn, none)
+    if (KR % 512 == 0) {
+      if (!bwd) { if (out_f32) FT_PIPE(false, true, true); else FT_PIPE(false, false, true); }
+      else { if (out_f32) FT_PIPE(true, true, true); else FT_PIPE(true, false, true); }
     } else {
-      if (out_f32) k_gemm_fp4_pipe<true, true, EPI_PLAIN><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out, tm, tn, none);
-      else k_gemm_fp4_pipe<true, false, EPI_PLAIN><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, out, tm, tn, none);
+      if (!bwd) { if (out_f32) FT_PIPE(false, true, false); else FT_PIPE(false, false, false); }
+      else { if (out_f32) FT_PIPE(true, true, false); else FT_PIPE(true, false, false); }
     }
+#undef FT_PIPE
     return hipGetLastError();
   }
   dim3 grid(tn, tm);
@@ -1098,8 +1141,14 @@ hipError_t launch_gemm_fp4_fused(bool bwd, const uint8_t* a, const uint8_t* as, 
   const int NO = bwd ? K : N;
   const int tm = (M + GB - 1) / GB, tn = (NO + GB - 1) / GB;
   const unsigned grid = (unsigned)(tm * tn);
-  if (!bwd) k_gemm_fp4_pipe<false, false, EPI_GELU><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, nullptr, tm, tn, ep);
-  else k_gemm_fp4_pipe<true, false, EPI_DGELU><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, nullptr, tm, tn, ep);
+  const bool sap = (bwd ? N : K) % 512 == 0;   // A scales in stage pairs
+  if (!bwd) {
+    if (sap) k_gemm_fp4_pipe<false, false, EPI_GELU, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, nullptr, tm, tn, ep);
+    else k_gemm_fp4_pipe<false, false, EPI_GELU, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, bias, nullptr, tm, tn, ep);
+  } else {
+    if (sap) k_gemm_fp4_pipe<true, false, EPI_DGELU, true><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, nullptr, tm, tn, ep);
+    else k_gemm_fp4_pipe<true, false, EPI_DGELU, false><<<grid, 256, 0, st>>>(a, as, wq, ws, M, N, K, P, R, lr, nullptr, nullptr, tm, tn, ep);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || ep.R2 == 0 || tn == 1) return e;
   return launch_reduce_parts(ep.parts, tn, (size_t)M * ep.R2, proj_out, 0, nullptr, false, st);

@@ -34,14 +34,57 @@ struct QuantLds {
   static constexpr int ROWS = MODE == 1 ? CW : RT * 32;
   static constexpr int PROJ_HW = MODE == 0 ? 0 : ROWS * STRIDE;
   static constexpr int X_HW = MODE == 0 ? 0 : 32 * QR_XSTRIDE;          // per wave
-  static constexpr int HALFWORDS = MODE == 0 ? 8 : PROJ_HW + WAVES * X_HW;
+  static constexpr int SC_ROW = CW / 32;                                 // scale bytes per row of a chunk
+  static constexpr int SC_HW = 32 * SC_ROW / 2;                          // per wave: 32 rows of scale bytes
+  static constexpr int HALFWORDS = PROJ_HW + WAVES * (X_HW + SC_HW);
 };
+
+typedef unsigned short v2u16 __attribute__((ext_vector_type(2)));
 
 // max over the 4 lanes of each aligned quad
 __device__ __forceinline__ uint32_t quad_max(uint32_t m) {
   m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0xB1, 0xF, 0xF, true));  // quad_perm [1,0,3,2]
   m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0x4E, 0xF, 0xF, true));  // quad_perm [2,3,0,1]
   return m;
+}
+
+// One 64-column step of a wave's 32 rows (4 groups of 8 rows): block
+// scales and codes, the scale bytes staged in the wave's LDS rows, and (XT)
+// the step's bf16 values in the wave's projection tile.  EDGE: rows past
+// the end and blocks past the chunk are zeroed and not stored.
+template <bool EDGE, bool XT>
+__device__ __forceinline__ void quant_step(const v4i (&x)[4], int rw0, int rows, bool col_ok, int lr, int lc,
+                                           int lane, uint8_t* const (&cptr)[4], int st, FT_LDS uint8_t* sc,
+                                           int sc_row, FT_LDS uint16_t* xt) {
+#pragma unroll
+  for (int q = 0; q < 4; q++) {
+    const int row = rw0 + 8 * q + lr;
+    const bool ok = !EDGE || (col_ok && row < rows);
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; e++) w[e] = ok ? (uint32_t)x[q][e] : 0u;
+    // largest |bf16| bit pattern: packed 16-bit maxima of the sign-cleared pairs
+    v2u16 p[4];
+#pragma unroll
+    for (int e = 0; e < 4; e++) p[e] = __builtin_bit_cast(v2u16, w[e] & 0x7FFF7FFFu);
+    const v2u16 pm = __builtin_elementwise_max(__builtin_elementwise_max(p[0], p[1]),
+                                               __builtin_elementwise_max(p[2], p[3]));
+    uint32_t m = max((uint32_t)pm[0], (uint32_t)pm[1]);
+    m = quad_max(m);
+    const uint32_t code = e8m0_from_amax_bits(m);
+    const float s = e8m0_to_f32(code);
+    uint32_t o = 0;
+    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[0]), s, 0);
+    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[1]), s, 1);
+    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[2]), s, 2);
+    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[3]), s, 3);
+    if (ok) *(uint32_t*)(cptr[q] + 32 * st) = o;
+    // scale bytes of (row, blocks 2st, 2st+1): the row's first lane takes the
+    // second quad's code along (row_shl:4) and writes both
+    const uint32_t code2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)code, 0x104, 0xF, 0xF, true);
+    if ((lane & 7) == 0) *(FT_LDS uint16_t*)(sc + (8 * q + lr) * sc_row + 2 * st) = (uint16_t)(code | (code2 << 8));
+    if constexpr (XT) *(FT_LDS v4i*)(xt + (8 * q + lr) * QR_XSTRIDE + lc) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+  }
 }
 
 template <int RT, int MODE, int WAVES, int CW>
@@ -109,7 +152,12 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
 #pragma unroll
   for (int t = 0; t < RT; t++) acc[t] = v16f{};
   FT_LDS uint16_t* xt = (FT_LDS uint16_t*)lds + L::PROJ_HW + wave * L::X_HW;  // this wave's 32x64 tile
+  FT_LDS uint8_t* sc = (FT_LDS uint8_t*)((FT_LDS uint16_t*)lds + L::PROJ_HW + WAVES * L::X_HW + wave * L::SC_HW);
   const int r32 = lane & 31, h = lane >> 5;
+  // code bytes of this lane's rows 8q + lr at the step's first column (steps add 32 bytes)
+  uint8_t* cptr[4];
+#pragma unroll
+  for (int q = 0; q < 4; q++) cptr[q] = codes + (size_t)(rw0 + 8 * q + lr) * (cols >> 1) + ((c0 + lc) >> 1);
 
 #pragma unroll
   for (int st = 0; st < NST; st++) {
@@ -117,36 +165,12 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
     if (st + PF < NST) issue(st + PF);
     const int blk = 2 * st + (lane >> 2 & 1);           // this lane's block within the chunk
     const bool col_ok = blk < nblk;
-#pragma unroll
-    for (int q = 0; q < 4; q++) {
-      const int row = rw0 + 8 * q + lr;
-      const bool ok = col_ok && row < rows;
-      uint32_t w[4];
-#pragma unroll
-      for (int e = 0; e < 4; e++) w[e] = ok ? (uint32_t)xv[st][q][e] : 0u;
-      uint32_t m = 0;
-#pragma unroll
-      for (int e = 0; e < 4; e++) {
-        const uint32_t a = w[e] & 0x7FFF7FFFu;
-        m = max(m, max(a & 0xFFFFu, a >> 16));
-      }
-      m = quad_max(m);
-      const uint32_t code = e8m0_from_amax_bits(m);
-      const float s = e8m0_to_f32(code);
-      uint32_t o = 0;
-      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[0]), s, 0);
-      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[1]), s, 1);
-      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[2]), s, 2);
-      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[3]), s, 3);
-      if (ok) {
-        const int col = c0 + 64 * st + lc;
-        *(uint32_t*)(codes + (size_t)row * (cols >> 1) + (col >> 1)) = o;
-        if ((lane & 3) == 0) scales[(size_t)row * nbc + (col >> 5)] = (uint8_t)code;
-      }
-      if constexpr (MODE != 0) {
-        *(FT_LDS v4i*)(xt + (8 * q + lr) * QR_XSTRIDE + lc) = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-      }
-    }
+    // interior (every row of the wave and both blocks of the step in range):
+    // no masking; the edge path zeroes what lies outside
+    if (rw0 + 32 > rows || 2 * st + 2 > nblk)
+      quant_step<true, MODE != 0>(xv[st], rw0, rows, col_ok, lr, lc, lane, cptr, st, sc, L::SC_ROW, xt);
+    else
+      quant_step<false, MODE != 0>(xv[st], rw0, rows, col_ok, lr, lc, lane, cptr, st, sc, L::SC_ROW, xt);
 
     if constexpr (MODE != 0) {
       const int g16 = lane >> 4, t16 = lane & 15;
@@ -170,6 +194,28 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
             b = make_v8bf(lo, hi);
           }
           acc[t] = mfma_bf16_32x32x16(a, b, acc[t]);
+        }
+      }
+    }
+  }
+
+  // scales: each row's bytes of this chunk are contiguous; 4-byte stores when
+  // rows and the chunk start are 4-byte aligned, else bytes
+  {
+    constexpr int DW = L::SC_ROW / 4;   // dwords per staged row
+    const bool al = (nbc & 3) == 0 && ((c0 >> 5) & 3) == 0;
+#pragma unroll
+    for (int d0 = 0; d0 < 32 * DW; d0 += 64) {
+      const int d = d0 + lane;
+      const int rr = d / DW, dw = d % DW;
+      const int row = rw0 + rr;
+      if (d < 32 * DW && row < rows && 4 * dw < nblk) {
+        uint8_t* dst = scales + (size_t)row * nbc + (c0 >> 5) + 4 * dw;
+        const FT_LDS uint8_t* srcb = sc + rr * L::SC_ROW + 4 * dw;
+        if (al && 4 * dw + 4 <= nblk) {
+          *(uint32_t*)dst = *(const FT_LDS uint32_t*)srcb;
+        } else {
+          for (int b = 0; b < 4 && 4 * dw + b < nblk; b++) dst[b] = srcb[b];
         }
       }
     }
