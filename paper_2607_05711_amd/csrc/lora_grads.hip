@@ -8,8 +8,8 @@
 // transposing 16-bit LDS read, L with 32-bit reads, split into two bf16 terms
 // (hi + lo) so that its ~16 leading bits take part.
 //
-// Workgroup = 4 waves over 128 output columns (32 per wave) and one chunk of
-// the token axis.  With several chunks each one stores its fp32 partial in a
+// Workgroup = 4 waves over 256 output columns (two 32-column tiles per wave,
+// sharing each hi/lo split of L) and one chunk of the token axis.  With several chunks each one stores its fp32 partial in a
 // workspace and a reduction kernel sums them in a fixed order.  Stages move through an LDS
 // ring with buffer loads that write LDS directly, one or two stages ahead of
 // the one on the matrix cores.  The two k-halves of an MFMA take the even and
@@ -21,10 +21,10 @@
 
 namespace ft {
 
-constexpr int LG_WC = 128;                    // output columns per workgroup
+constexpr int LG_WC = 256;                    // output columns per workgroup
 constexpr int LG_BM = 64;                     // token rows per stage
 constexpr int LG_VROW = LG_WC * 2;            // bytes per V row in LDS
-constexpr int LG_VBYTES = LG_BM * LG_VROW;    // 16 KB
+constexpr int LG_VBYTES = LG_BM * LG_VROW;    // 32 KB
 
 template <int RTJ>
 struct LoraGeom {
@@ -50,8 +50,8 @@ struct LoraJob {
   size_t part_off;      // offset of this output within a workspace part (floats)
 };
 
-// 16-byte chunk swizzle of a V row (16 chunks): rows 0..7 of a group spread
-// their chunks over all 16 positions.
+// 16-byte chunk swizzle of a V row (32 chunks): rows 0..7 of a group spread
+// their chunks over 16 positions.
 __device__ __forceinline__ int lg_swz(int row, int chunk) { return chunk ^ ((row & 7) << 1); }
 
 // One workgroup's share: output columns [c0, c0 + LG_WC) of `job` over token
@@ -69,14 +69,14 @@ __device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int 
   const uint32_t lds0 = lds_addr(lds);
 
   // Per-lane DMA sources.  V load i of this wave fills LDS bytes
-  // [1024 (4 wave + i), +1024) of the stage's V area: rows 4(4 wave + i) + lane/16,
-  // physical chunk lane%16 holding logical chunk lg_swz(row, lane%16).
+  // [1024 (8 wave + i), +1024) of the stage's V area: rows 2(8 wave + i) + lane/32,
+  // physical chunk lane%32 holding logical chunk lg_swz(row, lane%32).
   int v_row[G::V_LOADS];
   uint32_t v_src[G::V_LOADS];
 #pragma unroll
   for (int i = 0; i < G::V_LOADS; i++) {
-    const int row = 4 * (G::V_LOADS * wave + i) + (lane >> 4);
-    const int c = c0 + 8 * lg_swz(row, lane & 15);
+    const int row = 2 * (G::V_LOADS * wave + i) + (lane >> 5);
+    const int c = c0 + 8 * lg_swz(row, lane & 31);
     v_row[i] = row;
     v_src[i] = c < job.C ? (uint32_t)(row * job.C + c) * 2u : kOobOffset;
   }
@@ -104,17 +104,21 @@ __device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int 
 
   // LDS read offsets within a slot.  V: source lane (jj, qq) of 16-lane group
   // g16 reads row 2 jj + h (+8 for the second read, +16 per k-step) at
-  // logical column 32 wave + 16 (g16 & 1) + 4 qq.  L: lane (j, h) reads rows
-  // 2e + h (+16 per k-step) of column j.
+  // logical column 64 wave + 32 t2 + 16 (g16 & 1) + 4 qq for column tile t2.
+  // L: lane (j, h) reads rows 2e + h (+16 per k-step) of column j.
   const int g16 = lane >> 4, i16 = lane & 15, jj = i16 >> 2, qq = i16 & 3, h = g16 >> 1;
   const int vr0 = 2 * jj + h;
-  const int vcol = 32 * wave + 16 * (g16 & 1) + 4 * qq;
-  const uint32_t v_rd = (uint32_t)(vr0 * LG_VROW + lg_swz(vr0, vcol >> 3) * 16 + (vcol & 7) * 2);
+  uint32_t v_rd[2];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; t2++) {
+    const int vcol = 64 * wave + 32 * t2 + 16 * (g16 & 1) + 4 * qq;
+    v_rd[t2] = (uint32_t)(vr0 * LG_VROW + lg_swz(vr0, vcol >> 3) * 16 + (vcol & 7) * 2);
+  }
   const uint32_t l_rd = (uint32_t)(LG_VBYTES + h * G::LROW + 4 * (lane & 31));
 
-  v16f acc[RTJ];
+  v16f acc[RTJ][2];
 #pragma unroll
-  for (int t = 0; t < RTJ; t++) acc[t] = v16f{};
+  for (int t = 0; t < RTJ; t++) acc[t][0] = acc[t][1] = v16f{};
 
   issue(0);
   if (G::PD > 1 && nst > 1) issue(1);
@@ -129,8 +133,12 @@ __device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int 
     const FT_LDS uint8_t* sb = (const FT_LDS uint8_t*)lds + (s % G::NS) * G::SLOT;
 #pragma unroll
     for (int ks = 0; ks < 4; ks++) {
-      const FT_LDS uint8_t* vp = sb + v_rd + ks * 16 * LG_VROW;
-      const v8bf vf = make_v8bf(lds_read_tr16(vp), lds_read_tr16(vp + 8 * LG_VROW));
+      v8bf vf[2];
+#pragma unroll
+      for (int t2 = 0; t2 < 2; t2++) {
+        const FT_LDS uint8_t* vp = sb + v_rd[t2] + ks * 16 * LG_VROW;
+        vf[t2] = make_v8bf(lds_read_tr16(vp), lds_read_tr16(vp + 8 * LG_VROW));
+      }
 #pragma unroll
       for (int t = 0; t < RTJ; t++) {
         const FT_LDS float* lp = (const FT_LDS float*)(sb + l_rd + ks * 16 * G::LROW + t * 128);
@@ -143,12 +151,15 @@ __device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int 
           lo[e] = (int)lq;
         }
         const v8bf ah = __builtin_bit_cast(v8bf, hi), al = __builtin_bit_cast(v8bf, lo);
-        if constexpr (DB) {
-          acc[t] = mfma_bf16_32x32x16(ah, vf, acc[t]);
-          acc[t] = mfma_bf16_32x32x16(al, vf, acc[t]);
-        } else {
-          acc[t] = mfma_bf16_32x32x16(vf, ah, acc[t]);
-          acc[t] = mfma_bf16_32x32x16(vf, al, acc[t]);
+#pragma unroll
+        for (int t2 = 0; t2 < 2; t2++) {
+          if constexpr (DB) acc[t][t2] = mfma_bf16_32x32x16(ah, vf[t2], acc[t][t2]);
+          else acc[t][t2] = mfma_bf16_32x32x16(vf[t2], ah, acc[t][t2]);
+        }
+#pragma unroll
+        for (int t2 = 0; t2 < 2; t2++) {
+          if constexpr (DB) acc[t][t2] = mfma_bf16_32x32x16(al, vf[t2], acc[t][t2]);
+          else acc[t][t2] = mfma_bf16_32x32x16(vf[t2], al, acc[t][t2]);
         }
       }
     }
@@ -160,16 +171,18 @@ __device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int 
 #pragma unroll
   for (int t = 0; t < RTJ; t++)
 #pragma unroll
-    for (int v = 0; v < 16; v++) {
-      const int tr = 8 * (v >> 2) + 4 * h + (v & 3);
-      const int j = DB ? t * 32 + tr : t * 32 + l32;
-      const int c = c0 + 32 * wave + (DB ? l32 : tr);
-      if (j < r && c < job.C) {
-        const size_t idx = DB ? (size_t)j * job.C + c : (size_t)c * r + j;
-        if (part) part[job.part_off + idx] = acc[t][v];
-        else job.out[idx] = accumulate ? job.out[idx] + acc[t][v] : acc[t][v];
+    for (int t2 = 0; t2 < 2; t2++)
+#pragma unroll
+      for (int v = 0; v < 16; v++) {
+        const int tr = 8 * (v >> 2) + 4 * h + (v & 3);
+        const int j = DB ? t * 32 + tr : t * 32 + l32;
+        const int c = c0 + 64 * wave + 32 * t2 + (DB ? l32 : tr);
+        if (j < r && c < job.C) {
+          const size_t idx = DB ? (size_t)j * job.C + c : (size_t)c * r + j;
+          if (part) part[job.part_off + idx] = acc[t][t2][v];
+          else job.out[idx] = accumulate ? job.out[idx] + acc[t][t2][v] : acc[t][t2][v];
+        }
       }
-    }
 }
 
 // parts: nmch workspace parts of part_len floats, or NULL when one chunk covers
