@@ -363,10 +363,10 @@ def main():
     gemm = max(gemms, key=lambda k: step_us[k])
     per_call_flops = counts[gemm] / (calls[gemm] / psteps)
     achieved = counts[gemm] / (step_us[gemm] * 1e-6) / 1e12
-    kname = {"gemm_fwd": "ft::k_gemm_fp4_pipe<false, false, 0> (forward)",
-             "gemm_bwd": "ft::k_gemm_fp4_pipe<true, false, 0> (backward-input)",
-             "gemm_fwd_gelu": "ft::k_gemm_fp4_pipe<false, false, 1> (forward, GELU epilogue)",
-             "gemm_bwd_dgelu": "ft::k_gemm_fp4_pipe<true, false, 2> (backward-input, dGELU epilogue)"}[gemm]
+    kname = {"gemm_fwd": "ft::k_gemm_fp4_pipe<false, false, 0, true> (forward)",
+             "gemm_bwd": "ft::k_gemm_fp4_pipe<true, false, 0, true> (backward-input)",
+             "gemm_fwd_gelu": "ft::k_gemm_fp4_pipe<false, false, 1, true> (forward, GELU epilogue)",
+             "gemm_bwd_dgelu": "ft::k_gemm_fp4_pipe<true, false, 2, true> (backward-input, dGELU epilogue)"}[gemm]
     frac = {}
     for k in kinds:
         if k.startswith("gemm"):
