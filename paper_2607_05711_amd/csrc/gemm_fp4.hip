@@ -247,10 +247,13 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_generic(const uint8_t* __re
 //     bf16) or D chunk (backward, [256 k][32 j] bf16).  P is split into two
 //     bf16 terms in registers; its product lands in the same accumulators.
 // An FP4 stage runs as four k-steps of 16 MFMAs per wave (a low-rank stage
-// as two of 32), each carrying the LDS reads of the next.  Stage s+2 loads in
-// two parts: the first right after the barrier that publishes stage s+1 (the
-// slot of stage s is free from then on), the second during the first k-step
-// of stage s+1; the barrier before the last k-step of stage s+1 publishes it.
+// as two of 32), each carrying the LDS reads of the next.  The loads of stage
+// s+2 start right after the barrier that publishes stage s+1 (the slot of
+// stage s is free from then on) and spread over k-step 3 of stage s and
+// k-steps 0 and 1 of stage s+1, one load per two MFMAs at most: a load that
+// fills LDS holds its wave for about one MFMA's time when the four waves
+// issue loads back to back, much less when they are spaced.  The barrier
+// before the last k-step of stage s+1 publishes stage s+2.
 // The finished tile is staged through LDS for coalesced stores.
 
 constexpr int PK = 256;                  // reduction elements per FP4 stage
@@ -266,9 +269,6 @@ constexpr int OFF_SAP = 2 * 68 * 1024;   // after the two slots
 constexpr int SAP_SLOT = 256 * 16;       // bytes per stage pair; a third slot takes loads that do not apply
 constexpr int OFF_SB = 66 * 1024;        // W scales: 4 waves x 256 bytes
 constexpr int LR_COLS = 32;              // up-projection columns per low-rank stage
-// buffer loads per wave in the first part of a stage: FP4 (A tile, A scales), low-rank (P chunk)
-constexpr int LOADS_A = 10;
-constexpr int LOADS_P = 8;
 
 // Stage kinds, and a compile-time tag for the pipeline bodies.
 enum { SK_NONE = 0, SK_FP4 = 1, SK_LR = 2 };
@@ -570,10 +570,6 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
            BWD ? (uint32_t)t.u * 8 * nwkb : (uint32_t)t.u * 8);
     }
   };
-  // Loads of part 1 of stage u (the count a wait leaves outstanding).
-  auto part1_loads = [&](int u) {
-    return u >= total ? 0 : (u < nst ? ((SAP && (u & 1)) ? LOADS_A - 2 : LOADS_A) : LOADS_P);
-  };
   // Every load this wave issued has landed and its own LDS reads are done;
   // after the barrier the same holds for all waves.
   auto publish_all = [&]() {
@@ -709,11 +705,25 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   };
 
   // ---------------- pipeline
-  // Stage u: part 1 issued in iteration u-2 (after its barrier), part 2 in
-  // iteration u-1 (first k-step); stages 0 and 1 start here.
+  // Stage u: A-tile rows 0..3 of each wave's 8 and the A scales ("part 1a")
+  // issued in iteration u-2 after its barrier; A-tile rows 4..7 and the W
+  // tile and scales in iteration u-1 (k-steps 0 and 1).  Stage 0 and part 1a
+  // of stage 1 start here.
   issue_part1(0);
   issue_part2(0);
-  issue_part1(1);
+  if (1 < total) {
+    if (1 < nst) {
+      const bool hf = half_last && 1 == nst - 1;
+#pragma unroll
+      for (int v = 0; v < 4; v++) fp4_part1_one(1, v, hf);
+      fp4_part1_one(1, 8, hf);
+      fp4_part1_one(1, 9, hf);
+    } else {
+      const bool hf = half_lr && 1 == total - 1;
+#pragma unroll
+      for (int v = 0; v < 4; v++) lr_part1_one(1, v, hf);
+    }
+  }
   // Accumulators start at the bias (forward): every output's sum begins with
   // its bias term, in both output precisions.
 #pragma unroll
@@ -727,9 +737,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         acc[i][j][4 * q + 2] = bf16_to_f32(bias4[j][q].y & 0xFFFFu);
         acc[i][j][4 * q + 3] = bf16_to_f32(bias4[j][q].y >> 16);
       }
-  switch (part1_loads(1)) {   // stage 0 landed; part 1 of stage 1 may stay in flight
-    case LOADS_A: wait_vm<LOADS_A>(); break;
-    case LOADS_P: wait_vm<LOADS_P>(); break;
+  // stage 0 landed; part 1a of stage 1 (4 tile loads, plus 2 scale loads
+  // without paired A scales: stage 1's pair loaded with stage 0) may stay in flight
+  switch (1 >= total ? 0 : (1 < nst && !SAP ? 6 : 4)) {
+    case 4: wait_vm<4>(); break;
+    case 6: wait_vm<6>(); break;
     default: wait_vm<0>(); break;
   }
   __builtin_amdgcn_s_barrier();
@@ -750,11 +762,15 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   // not).  Every other instruction sits between two MFMAs (one wave per SIMD:
   // the matrix pipe only stays busy if nothing waits in front of the next
   // MFMA):
-  //   k-step 0 carries the reads of k-step 1 and part 2 of stage s+1;
-  //   k-steps 1, 2 carry the reads of k-steps 2, 3;
+  //   k-step 0 carries the reads of k-step 1, A-tile rows 4..7 and W-tile
+  //   rows 0..3 of stage s+1;
+  //   k-step 1 carries the reads of k-step 2, W-tile rows 4..7 and the W
+  //   scales of stage s+1;
+  //   k-step 2 carries the reads of k-step 3;
   //   the barrier publishes stage s+1 and frees the slot of stage s;
-  //   k-step 3 carries the reads of stage s+1's k-step 0 and scales, part 1
-  //   of stage s+2, and the scale operands of stage s+1.
+  //   k-step 3 carries the reads of stage s+1's k-step 0 and scales, part 1a
+  //   of stage s+2 (A-tile rows 0..3, A scales), and the scale operands of
+  //   stage s+1.
   // PAR (whole stages only): the parity of s, which decides whether k-step 3
   // loads a pair of A-scale stages (SAP).
   auto fp4_body = [&](int s, auto anyc, auto parc) {
@@ -768,9 +784,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       const int i = m >> 2, j = m & 3;
       acc[i][j] = mfma_fp4_32x32x64<0>(f0.b[j], f0.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
       if (m < FRAG_READS) read_one(s, 1, m, f1);
-      if (m < 9) {
-        if constexpr (ANY) any_part2_one(t2, m);
-        else fp4_part2_one(s + 1, m, false);
+      if ((m & 3) == 0) {
+        const int v = 4 + (m >> 2);
+        if constexpr (ANY) any_part1_one(t2, v);
+        else fp4_part1_one(s + 1, v, false);
+      } else if ((m & 3) == 2) {
+        const int v = m >> 2;
+        if constexpr (ANY) any_part2_one(t2, v);
+        else fp4_part2_one(s + 1, v, false);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -779,6 +800,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       const int i = m >> 2, j = m & 3;
       acc[i][j] = mfma_fp4_32x32x64<1>(f1.b[j], f1.a[i], acc[i][j], (int)sb[j], (int)sa[i]);
       if (m < FRAG_READS) read_one(s, 2, m, f0);
+      if ((m & 3) == 0 || m == 2) {
+        const int v = m == 2 ? 8 : 4 + (m >> 2);
+        if constexpr (ANY) any_part2_one(t2, v);
+        else fp4_part2_one(s + 1, v, false);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
@@ -798,14 +824,15 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       if (m < FRAG_READS) read_one(s + 1, 0, m, f0);
       if (m == FRAG_READS - 4) read_scales_a(s + 1, sr);
       if (m == FRAG_READS - 2) read_scales_b(nslot, sr);
-      if (m < 10) {
+      if ((m & 3) == 0 || m == 2 || m == 6) {
+        const int v = m == 2 ? 8 : m == 6 ? 9 : m >> 2;
         if constexpr (ANY) {
-          any_part1_one(t1, m);
+          any_part1_one(t1, v);
         } else if constexpr (SAP) {
-          if (m < 8) fp4_part1_one(s + 2, m, false);
-          else if (m == 8 && PAR == 0) pair_load(s + 2, true);
+          if (v < 8) fp4_part1_one(s + 2, v, false);
+          else if (v == 8 && PAR == 0) pair_load(s + 2, true);
         } else {
-          fp4_part1_one(s + 2, m, false);
+          fp4_part1_one(s + 2, v, false);
         }
       }
       if (m == 15) scale_ops(sr, nsa, nsb);
@@ -817,12 +844,15 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
 
   // One low-rank iteration (stage s >= nst, its first half in ga):
   //   half 0: 32 MFMAs carrying the hi/lo splits of its row tiles 1..3, the
-  //   reads of half 1 and part 2 of stage s+1;
+  //   reads of half 1, and P rows 4..7 and the U / D chunk of stage s+1;
   //   the barrier publishes stage s+1 and frees the slot of stage s;
-  //   half 1: likewise, carrying part 1 of stage s+2 and the reads of stage
-  //   s+1's first half (unused past the last stage).
-  // The second half of a 16-column last stage reads as zeros and adds zeros.
-  auto lr_body = [&](int s) {
+  //   half 1: likewise, carrying part 1a of stage s+2 (P rows 0..3) and the
+  //   reads of stage s+1's first half (unused past the last stage).
+  // P2 / P1: stage s+1 / s+2 exists (no loads are issued for stages past
+  // the end).  The second half of a 16-column last stage reads as zeros and
+  // adds zeros.
+  auto lr_body = [&](int s, auto p2c, auto p1c) {
+    constexpr bool P2 = decltype(p2c)::value != 0, P1 = decltype(p1c)::value != 0;
     const StageSel t2 = stage_sel(s + 1), t1 = stage_sel(s + 2);
     LrOps o;
 #pragma unroll
@@ -833,7 +863,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       lr_mfma(m, ga, o);
       if (m < 12) lr_split(ga, (m >> 2) + 1, m & 3, o);
       if (m >= 16 && m - 16 < LR_READS) lr_read_one(s, 1, m - 16, gb);
-      if (m < 4) any_part2_one(t2, m);
+      if constexpr (P2) {
+        if ((m & 3) == 0 && m < 16) any_part1_one(t2, 4 + (m >> 2));
+        else if ((m & 3) == 2 && m < 16) any_part2_one(t2, m >> 2);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
     publish_all();
@@ -845,7 +878,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     for (int m = 0; m < 32; m++) {
       lr_mfma(m, gb, o);
       if (m < 12) lr_split(gb, (m >> 2) + 1, m & 3, o);
-      if (m < 8) any_part1_one(t1, m);
+      if constexpr (P1) { if ((m & 3) == 0 && m < 16) any_part1_one(t1, m >> 2); }
       if (m >= 16 && m - 16 < LR_READS) lr_read_one(s + 1, 0, m - 16, ga);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -866,7 +899,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
 #pragma unroll
     for (int q = 0; q < LR_READS; q++) lr_read_one(nst, 0, q, ga);
 #pragma unroll 1
-    for (; s < total; s++) lr_body(s);
+    for (; s < total - 2; s++) lr_body(s, IC<1>{}, IC<1>{});
+    if (s < total - 1) lr_body(s++, IC<1>{}, IC<0>{});
+    lr_body(s++, IC<0>{}, IC<0>{});
   }
 
   // ---------------- epilogue: convert, store
