@@ -107,8 +107,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
   const int nbc = cols >> 5;
   const int lr = lane >> 3, lc = (lane & 7) * 8;     // row within an 8-row group, column within a step
 
-  // The first PF steps' loads go out before anything else; each step, once
-  // consumed, issues the load PF steps ahead.  Rows past the end and blocks
+  // The first PF steps' loads go out right after the projection chunk's;
+  // each step, once consumed, issues the load PF steps ahead.  Rows past the end and blocks
   // past the chunk read an in-range address; their values become zeros.
   constexpr int PF = NST < 6 ? NST : 6;
   v4i xv[NST][4];
@@ -120,15 +120,14 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
       xv[st][q] = *(const v4i*)(src + (size_t)row * cols + c0 + col);
     }
   };
-#pragma unroll
-  for (int st = 0; st < PF; st++) issue(st);
-
+  // The projection chunk is loaded first: every step's MFMAs need it, while
+  // the steps' own rows arrive one after another behind it.  It is staged
+  // in LDS as 16-byte slots, zero outside [R] x [ncols].
+  constexpr int SLOTS_PER_ROW = MODE == 1 ? RT * 4 : CW / 8;
+  constexpr int NSLOTS = L::ROWS * SLOTS_PER_ROW;
+  constexpr int PER_THREAD = MODE == 0 ? 1 : (NSLOTS + NT - 1) / NT;
+  [[maybe_unused]] uint4 v[PER_THREAD];
   if constexpr (MODE != 0) {
-    // Stage the projection chunk: 16-byte slots, zero outside [R] x [ncols].
-    constexpr int SLOTS_PER_ROW = MODE == 1 ? RT * 4 : CW / 8;
-    constexpr int NSLOTS = L::ROWS * SLOTS_PER_ROW;
-    constexpr int PER_THREAD = (NSLOTS + NT - 1) / NT;
-    uint4 v[PER_THREAD];
 #pragma unroll
     for (int u = 0; u < PER_THREAD; u++) {
       const int s = tid + NT * u;
@@ -140,6 +139,11 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
         if (s < NSLOTS && rr < R && cc < ncols) v[u] = *(const uint4*)(proj + (size_t)rr * cols + c0 + cc);
       }
     }
+  }
+#pragma unroll
+  for (int st = 0; st < PF; st++) issue(st);
+
+  if constexpr (MODE != 0) {
 #pragma unroll
     for (int u = 0; u < PER_THREAD; u++) {
       const int s = tid + NT * u;
