@@ -70,23 +70,27 @@ __device__ __forceinline__ float e8m0_to_f32(uint32_t code) {
 }
 
 // tanh-approximated GELU, 0.5 z (1 + tanh(u)) with u = c0 (z + c1 z^3), and
-// its derivative, in fp32.  With e = exp(-2|u|) (hardware exp2):
-//   1 + tanh(u) = 2 / (1 + e) for u >= 0, 2e / (1 + e) for u < 0,
-//   1 - tanh(u)^2 = 4e / (1 + e)^2,
-// which avoids the cancellation of 1 + tanh(u) for very negative z.
-constexpr float kGeluC0 = 0.7978845608028654f;   // sqrt(2 / pi)
-constexpr float kGeluC1 = 0.044715f;
-struct GeluParts { float one_plus_t, one_minus_t2; };
-__device__ __forceinline__ GeluParts gelu_parts(float z) {
-  const float u = kGeluC0 * (z + kGeluC1 * z * z * z);
-  const float e = __builtin_amdgcn_exp2f(-2.8853900817779268f * fabsf(u));   // exp(-2|u|)
+// its derivative, in fp32.  u has the sign of z; with
+// e = exp(-2|u|) = 2^(|z| (a + b z^2)), a = -2 c0 log2(e), b = a c1 (e <= 1,
+// so it never overflows) and r = 1 / (1 + e):
+//   0.5 (1 + tanh u) = r for z >= 0, e r for z < 0;   1 - tanh(u)^2 = 4 e r^2;
+//   GELU(z)  = z r or z e r (no cancellation for very negative z),
+//   GELU'(z) = 0.5 (1 + tanh u) + z e r^2 (2 c0 + 6 c0 c1 z^2).
+constexpr float kGeluA = -2.302208198e+00f;   // -2 sqrt(2/pi) log2(e)
+constexpr float kGeluB = -1.029432396e-01f;   // kGeluA * 0.044715
+constexpr float kGeluG1 = 1.595769122e+00f;  // 2 sqrt(2/pi)
+constexpr float kGeluG3 = 2.140644488e-01f;  // 6 sqrt(2/pi) 0.044715
+__device__ __forceinline__ float gelu_tanh(float z) {
+  const float e = __builtin_amdgcn_exp2f(fabsf(z) * fmaf(kGeluB, z * z, kGeluA));
   const float r = __builtin_amdgcn_rcpf(1.0f + e);   // hardware reciprocal (1 ulp)
-  return {(u >= 0.0f ? 2.0f : 2.0f * e) * r, 4.0f * e * r * r};
+  return (z >= 0.0f ? z : z * e) * r;
 }
-__device__ __forceinline__ float gelu_tanh(float z) { return 0.5f * z * gelu_parts(z).one_plus_t; }
 __device__ __forceinline__ float gelu_tanh_grad(float z) {
-  const GeluParts g = gelu_parts(z);
-  return 0.5f * g.one_plus_t + 0.5f * z * g.one_minus_t2 * kGeluC0 * (1.0f + 3.0f * kGeluC1 * z * z);
+  const float t = z * z;
+  const float e = __builtin_amdgcn_exp2f(fabsf(z) * fmaf(kGeluB, t, kGeluA));
+  const float r = __builtin_amdgcn_rcpf(1.0f + e);
+  const float er = e * r;
+  return fmaf(z * er * r, fmaf(kGeluG3, t, kGeluG1), z >= 0.0f ? r : er);
 }
 
 // Quantize 8 consecutive bf16 (packed in w) of a 32-element block held by a

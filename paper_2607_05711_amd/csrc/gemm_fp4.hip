@@ -976,6 +976,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     uint8_t* stg = lds + wave * STG;
     uint16_t* ps = (uint16_t*)(lds + 4 * STG);
     float* comb = (float*)(lds + 4 * STG + PSLICE);          // [2 buffers][2 pairs][32 rows][64]
+    // E8M0 codes of this wave's 128 rows x 4 blocks, written out once at the end
+    uint8_t* sbuf = lds + 4 * STG + PSLICE + 2 * 2 * 32 * 64 * 4 + wave * 512;
+    static_assert(4 * STG + PSLICE + 2 * 2 * 32 * 64 * 4 + 4 * 512 <= NSLOT * SLOT, "epilogue LDS");
     const int R2 = ep.R2;
     const int tn = nt;
     __syncthreads();  // all waves are done with the ring
@@ -1073,7 +1076,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         uint32_t sc;
         const uint32_t codes = quad_quantize8(w, sc);
         __builtin_amdgcn_raw_buffer_store_b32((int)codes, r_q, inb ? (uint32_t)gr * (NO / 2) + gc / 2 : kOobOffset, 0, 0);
-        if (inb && (lane & 3) == 0) ep.s[(size_t)gr * (NO / 32) + gc / 32] = (uint8_t)sc;
+        if ((lane & 3) == 0) sbuf[(32 * i + rl) * 4 + (seg >> 2)] = (uint8_t)sc;
       }
       if (R2 == 0) continue;
       __builtin_amdgcn_s_waitcnt(0xc07f);
@@ -1106,15 +1109,39 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       }
       __syncthreads();
       if (wn == 0) {
-        float* dst = tiles_n > 1 ? ep.parts + (size_t)tn * M * R2 : ep.parts;
+        // the pair's sum in place, then out as 16-byte row segments
 #pragma unroll
         for (int t = 0; t < 2; t++)
 #pragma unroll
           for (int v = 0; v < 16; v++) {
             const int rr = 8 * (v >> 2) + 4 * h + (v & 3), j = 32 * t + r32;
-            const int gr = orow0 + 32 * i + rr;
-            if (j < R2 && gr < M) dst[(size_t)gr * R2 + j] = pacc[t][v] + cb[rr * 64 + j];
+            cb[rr * 64 + j] += pacc[t][v];
           }
+        float* dst = tiles_n > 1 ? ep.parts + (size_t)tn * M * R2 : ep.parts;
+#pragma unroll
+        for (int q = 0; q < 8; q++) {
+          const int rr = 4 * q + (lane >> 4), j = 4 * (lane & 15);
+          const int gr = orow0 + 32 * i + rr;
+          if (j < R2 && gr < M) *(float4*)(dst + (size_t)gr * R2 + j) = *(const float4*)(cb + rr * 64 + j);
+        }
+      }
+    }
+    // E8M0 codes: each lane writes rows lane and lane + 64 of the wave's 128,
+    // four blocks (one dword) per row when aligned and inside the matrix
+    const bool s_al = ((NO >> 5) & 3) == 0 && ocol0 + 128 <= NO;
+#pragma unroll
+    for (int k = 0; k < 2; k++) {
+      const int rr = lane + 64 * k, gr = orow0 + rr;
+      const uint32_t v = *(const uint32_t*)(sbuf + rr * 4);
+      if (gr < M) {
+        uint8_t* d = ep.s + (size_t)gr * (NO >> 5) + (ocol0 >> 5);
+        if (s_al) {
+          *(uint32_t*)d = v;
+        } else {
+#pragma unroll
+          for (int b = 0; b < 4; b++)
+            if (ocol0 + 32 * b < NO) d[b] = (uint8_t)(v >> (8 * b));
+        }
       }
     }
   }
