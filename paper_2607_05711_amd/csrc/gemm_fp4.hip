@@ -975,10 +975,15 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     constexpr int PSLICE = G ? 256 * PS1 * 2 : 64 * PS2 * 2;
     uint8_t* stg = lds + wave * STG;
     uint16_t* ps = (uint16_t*)(lds + 4 * STG);
-    float* comb = (float*)(lds + 4 * STG + PSLICE);          // [2 buffers][2 pairs][32 rows][64]
-    // E8M0 codes of this wave's 128 rows x 4 blocks, written out once at the end
-    uint8_t* sbuf = lds + 4 * STG + PSLICE + 2 * 2 * 32 * 64 * 4 + wave * 512;
-    static_assert(4 * STG + PSLICE + 2 * 2 * 32 * 64 * 4 + 4 * 512 <= NSLOT * SLOT, "epilogue LDS");
+    // This wave's E8M0 codes (128 rows x 4 blocks) and, for EPI_GELU, its
+    // E2M1 codes (128 rows x 64 bytes), written out once after the passes.
+    constexpr bool QLDS = G;
+    uint8_t* sbuf = lds + 4 * STG + PSLICE + wave * 512;
+    uint8_t* qbuf = lds + 4 * STG + PSLICE + 4 * 512 + wave * (128 * 64);
+    static_assert(4 * STG + PSLICE + 4 * 512 + (QLDS ? 4 * 128 * 64 : 0) <= NSLOT * SLOT, "epilogue LDS");
+    // After the passes, the projection partials of the two waves that share
+    // rows are added in [2 row halves][128 rows][64] fp32 at the start of LDS.
+    static_assert(2 * 128 * 64 * 4 <= 4 * STG + PSLICE, "combine area below the code buffers");
     const int R2 = ep.R2;
     const int tn = nt;
     __syncthreads();  // all waves are done with the ring
@@ -1075,13 +1080,16 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         *(v4i*)(srow + seg * 16) = wv;   // bf16 result in place (for the projection)
         uint32_t sc;
         const uint32_t codes = quad_quantize8(w, sc);
-        __builtin_amdgcn_raw_buffer_store_b32((int)codes, r_q, inb ? (uint32_t)gr * (NO / 2) + gc / 2 : kOobOffset, 0, 0);
+        if constexpr (QLDS) *(uint32_t*)(qbuf + (32 * i + rl) * 64 + seg * 4) = codes;
+        else __builtin_amdgcn_raw_buffer_store_b32((int)codes, r_q, inb ? (uint32_t)gr * (NO / 2) + gc / 2 : kOobOffset, 0, 0);
         if ((lane & 3) == 0) sbuf[(32 * i + rl) * 4 + (seg >> 2)] = (uint8_t)sc;
       }
       if (R2 == 0) continue;
       __builtin_amdgcn_s_waitcnt(0xc07f);
-      // 3) projection of the pass's 32 rows over this wave's 128 columns
-      v16f pacc[2] = {v16f{}, v16f{}};
+      // 3) projection of the pass's 32 rows over this wave's 128 columns, into
+      //    the pass's first two accumulator tiles (read out in step 1)
+      acc[i][0] = v16f{};
+      acc[i][1] = v16f{};
 #pragma unroll
       for (int ks = 0; ks < 8; ks++) {
         const v8bf a = __builtin_bit_cast(v8bf, *(const v4i*)(stg + r32 * SROW + (16 * ks + 8 * h) * 2));
@@ -1096,34 +1104,52 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
           } else {
             b = __builtin_bit_cast(v8bf, *(const v4i*)(ps + (32 * t + r32) * PS2 + kloc));
           }
-          pacc[t] = mfma_bf16_32x32x16(a, b, pacc[t]);
+          acc[i][t] = mfma_bf16_32x32x16(a, b, acc[i][t]);
         }
       }
-      // 4) the two waves with these rows (wn = 0, 1) add their partials
-      float* cb = comb + ((i & 1) * 2 + wm) * (32 * 64);
+    }
+    if (R2 > 0) {
+      // 4) the two waves with the same rows (wn = 0, 1) add their partials,
+      //    all passes at once, in LDS the passes no longer use; each then
+      //    stores half of the summed rows as 16-byte segments
+      __syncthreads();
+      float* cb = (float*)lds + wm * (128 * 64);
       if (wn == 1) {
 #pragma unroll
-        for (int t = 0; t < 2; t++)
+        for (int i = 0; i < 4; i++)
 #pragma unroll
-          for (int v = 0; v < 16; v++) cb[(8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * t + r32] = pacc[t][v];
+          for (int t = 0; t < 2; t++)
+#pragma unroll
+            for (int v = 0; v < 16; v++)
+              cb[(32 * i + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * t + r32] = acc[i][t][v];
       }
       __syncthreads();
       if (wn == 0) {
-        // the pair's sum in place, then out as 16-byte row segments
 #pragma unroll
-        for (int t = 0; t < 2; t++)
+        for (int i = 0; i < 4; i++)
 #pragma unroll
-          for (int v = 0; v < 16; v++) {
-            const int rr = 8 * (v >> 2) + 4 * h + (v & 3), j = 32 * t + r32;
-            cb[rr * 64 + j] += pacc[t][v];
-          }
-        float* dst = tiles_n > 1 ? ep.parts + (size_t)tn * M * R2 : ep.parts;
+          for (int t = 0; t < 2; t++)
 #pragma unroll
-        for (int q = 0; q < 8; q++) {
-          const int rr = 4 * q + (lane >> 4), j = 4 * (lane & 15);
-          const int gr = orow0 + 32 * i + rr;
-          if (j < R2 && gr < M) *(float4*)(dst + (size_t)gr * R2 + j) = *(const float4*)(cb + rr * 64 + j);
-        }
+            for (int v = 0; v < 16; v++)
+              cb[(32 * i + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * t + r32] += acc[i][t][v];
+      }
+      __syncthreads();
+      float* dst = tiles_n > 1 ? ep.parts + (size_t)tn * M * R2 : ep.parts;
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int rr = 64 * wn + 4 * q + (lane >> 4), j = 4 * (lane & 15);
+        const int gr = orow0 + rr;
+        if (j < R2 && gr < M) *(float4*)(dst + (size_t)gr * R2 + j) = *(const float4*)(cb + rr * 64 + j);
+      }
+    }
+    // E2M1 codes (EPI_GELU): 16 bytes (32 columns) of a row per lane
+    if constexpr (QLDS) {
+#pragma unroll
+      for (int q = 0; q < 8; q++) {
+        const int rr = 16 * q + (lane >> 2), c = lane & 3;
+        const int gr = orow0 + rr;
+        if (gr < M && ocol0 + 32 * c < NO)
+          *(v4i*)(ep.q + (size_t)gr * (NO / 2) + (ocol0 / 2) + 16 * c) = *(const v4i*)(qbuf + rr * 64 + 16 * c);
       }
     }
     // E8M0 codes: each lane writes rows lane and lane + 64 of the wave's 128,
