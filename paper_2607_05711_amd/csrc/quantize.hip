@@ -280,19 +280,22 @@ __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict_
 
 // ---------------------------------------------------------------- launchers
 // Geometry per mode, from timing at the FLUX shapes: 8 waves (256 rows) per
-// workgroup amortize the staged projection chunk; the [cols, R] projection
-// takes 256-column chunks (more workgroups than CUs for 4608 rows: 16.5 us
-// against 17.6 with 384), the [R, cols] one 768-column chunks (fewer
-// partial sums; 384 and 512 are slower) while the chunk fits LDS.
-static int quant_chunk_cols(int R, int layout) {
+// workgroup amortize the staged projection chunk.  The [cols, R] projection
+// takes 384-column chunks, or 256 when that would leave fewer workgroups
+// than CUs (4608 x 3072: 16.5 us against 17.6); more chunks mean more
+// partial sums, which dominate for long rows.  The [R, cols] projection
+// takes 768-column chunks (fewer partial sums; 384 and 512 are slower)
+// while the chunk fits LDS.
+static int quant_chunk_cols(int rows, int cols, int R, int layout) {
   if (R == 0) return 384;
-  if (layout == 0) return 256;
+  if (layout == 0) return (size_t)((rows + 255) / 256) * ((cols + 383) / 384) < 256 ? 256 : 384;
   return (R + 31) / 32 <= 2 ? 768 : 384;
 }
 
 size_t quant_rows_workspace(int rows, int cols, int R, int layout) {
   if (R == 0) return 0;
-  const int chunks = (cols + quant_chunk_cols(R, layout) - 1) / quant_chunk_cols(R, layout);
+  const int cw = quant_chunk_cols(rows, cols, R, layout);
+  const int chunks = (cols + cw - 1) / cw;
   return chunks > 1 ? (size_t)chunks * rows * R * sizeof(float) : 0;
 }
 
@@ -313,11 +316,19 @@ hipError_t launch_quant_rows(const uint16_t* src, int rows, int cols, uint8_t* c
     return launch_rows_t<1, 0, 4, 384>(src, rows, cols, codes, scales, nullptr, 0, nullptr, nullptr, st);
   const int rt = (R + 31) / 32;
   if (layout == 0) {
+    if (quant_chunk_cols(rows, cols, R, layout) == 256) {
+      switch (rt) {
+        case 1: return launch_rows_t<1, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+        case 2: return launch_rows_t<2, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+        case 3: return launch_rows_t<3, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+        default: return launch_rows_t<4, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+      }
+    }
     switch (rt) {
-      case 1: return launch_rows_t<1, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-      case 2: return launch_rows_t<2, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-      case 3: return launch_rows_t<3, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-      default: return launch_rows_t<4, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+      case 1: return launch_rows_t<1, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+      case 2: return launch_rows_t<2, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+      case 3: return launch_rows_t<3, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+      default: return launch_rows_t<4, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
     }
   }
   switch (rt) {

@@ -96,7 +96,9 @@ def test_quantize_tiles_bitexact(rows, cols):
 
 @pytest.mark.parametrize("rows,cols,R,layout", [(128, 256, 32, 0), (300, 640, 48, 0), (129, 1184, 64, 0),
                                                 (200, 416, 128, 0), (128, 256, 32, 1), (300, 800, 96, 1),
-                                                (77, 4096, 16, 1), (513, 384, 112, 0)])
+                                                (77, 4096, 16, 1), (513, 384, 112, 0),
+                                                # enough workgroups for 384-column chunks, ragged last one
+                                                (2304, 10976, 64, 0)])
 def test_quantize_fused_projection(rows, cols, R, layout):
     rng = np.random.default_rng(rows + cols + R)
     bits = random_rows("outliers", rows, cols, seed=rows)
