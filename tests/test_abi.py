@@ -80,9 +80,10 @@ def test_quantize_validation():
     assert q(NULL, 0, 64, 1, NULL, NULL) == _lib.FT_OK
     # a projection over several column chunks needs the workspace the size query reports
     need = _lib.ft_quantize_workspace_size(4608, 3072, 1, 64, 0)
-    assert need == 8 * 4608 * 64 * 4                       # 384-column chunks of [cols, R] projections
+    assert need == 12 * 4608 * 64 * 4      # 256-column chunks: 384 would leave fewer workgroups than CUs
+    assert _lib.ft_quantize_workspace_size(18432, 15360, 1, 96, 0) == 40 * 18432 * 96 * 4   # 384 otherwise
     assert _lib.ft_quantize_workspace_size(4608, 9216, 1, 64, 1) == 12 * 4608 * 64 * 4   # 768 for [R, cols]
-    assert _lib.ft_quantize_workspace_size(4608, 384, 1, 64, 0) == 0                     # one chunk: none
+    assert _lib.ft_quantize_workspace_size(4608, 256, 1, 64, 0) == 0                     # one chunk: none
     assert _lib.ft_quantize_workspace_size(4608, 3072, 1, 0, 0) == 0                     # no projection: none
     assert _lib.ft_quantize_workspace_size(4608, 3072, 32, 0, 0) == 0
     big = (ALIGNED, 4608, 3072, 1, ALIGNED, ALIGNED, ALIGNED2, 64, 0, ALIGNED2)
