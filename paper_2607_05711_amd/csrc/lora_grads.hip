@@ -130,36 +130,52 @@ __device__ __forceinline__ void lora_tile(const LoraJob& job, uint8_t* lds, int 
     asm volatile("" ::: "memory");  // no LDS read moves above the barrier
     if (s + G::PD < nst) issue(s + G::PD);
 
+    // All of the stage's fragments are read first and the MFMAs follow: with
+    // one wave per SIMD nothing else hides an LDS round trip, so the reads
+    // must not be interleaved with the arithmetic that consumes them.
     const FT_LDS uint8_t* sb = (const FT_LDS uint8_t*)lds + (s % G::NS) * G::SLOT;
+    v8bf vf[4][2];
+    float lv[4][RTJ][8];
 #pragma unroll
     for (int ks = 0; ks < 4; ks++) {
-      v8bf vf[2];
 #pragma unroll
       for (int t2 = 0; t2 < 2; t2++) {
         const FT_LDS uint8_t* vp = sb + v_rd[t2] + ks * 16 * LG_VROW;
-        vf[t2] = make_v8bf(lds_read_tr16(vp), lds_read_tr16(vp + 8 * LG_VROW));
+        vf[ks][t2] = make_v8bf(lds_read_tr16(vp), lds_read_tr16(vp + 8 * LG_VROW));
       }
 #pragma unroll
       for (int t = 0; t < RTJ; t++) {
         const FT_LDS float* lp = (const FT_LDS float*)(sb + l_rd + ks * 16 * G::LROW + t * 128);
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          lv[ks][t][2 * e] = lp[4 * e * (G::LROW / 4)];
+          lv[ks][t][2 * e + 1] = lp[(4 * e + 2) * (G::LROW / 4)];
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ks = 0; ks < 4; ks++) {
+#pragma unroll
+      for (int t = 0; t < RTJ; t++) {
         v4i hi, lo;
 #pragma unroll
         for (int e = 0; e < 4; e++) {
           uint32_t hp, lq;
-          split_bf16x2(lp[4 * e * (G::LROW / 4)], lp[(4 * e + 2) * (G::LROW / 4)], hp, lq);
+          split_bf16x2(lv[ks][t][2 * e], lv[ks][t][2 * e + 1], hp, lq);
           hi[e] = (int)hp;
           lo[e] = (int)lq;
         }
         const v8bf ah = __builtin_bit_cast(v8bf, hi), al = __builtin_bit_cast(v8bf, lo);
 #pragma unroll
         for (int t2 = 0; t2 < 2; t2++) {
-          if constexpr (DB) acc[t][t2] = mfma_bf16_32x32x16(ah, vf[t2], acc[t][t2]);
-          else acc[t][t2] = mfma_bf16_32x32x16(vf[t2], ah, acc[t][t2]);
+          if constexpr (DB) acc[t][t2] = mfma_bf16_32x32x16(ah, vf[ks][t2], acc[t][t2]);
+          else acc[t][t2] = mfma_bf16_32x32x16(vf[ks][t2], ah, acc[t][t2]);
         }
 #pragma unroll
         for (int t2 = 0; t2 < 2; t2++) {
-          if constexpr (DB) acc[t][t2] = mfma_bf16_32x32x16(al, vf[t2], acc[t][t2]);
-          else acc[t][t2] = mfma_bf16_32x32x16(vf[t2], al, acc[t][t2]);
+          if constexpr (DB) acc[t][t2] = mfma_bf16_32x32x16(al, vf[ks][t2], acc[t][t2]);
+          else acc[t][t2] = mfma_bf16_32x32x16(vf[ks][t2], al, acc[t][t2]);
         }
       }
     }
