@@ -52,9 +52,9 @@ __device__ __forceinline__ uint32_t quad_max(uint32_t m) {
 // scales and codes, the scale bytes staged in the wave's LDS rows, and (XT)
 // the step's bf16 values in the wave's projection tile.  EDGE: rows past
 // the end and blocks past the chunk are zeroed and not stored.
-template <bool EDGE, bool XT>
+template <bool EDGE, bool XT, class Store>
 __device__ __forceinline__ void quant_step(const v4i (&x)[4], int rw0, int rows, bool col_ok, int lr, int lc,
-                                           int lane, uint8_t* const (&cptr)[4], int st, FT_LDS uint8_t* sc,
+                                           int lane, const Store& store, int st, FT_LDS uint8_t* sc,
                                            int sc_row, FT_LDS uint16_t* xt) {
 #pragma unroll
   for (int q = 0; q < 4; q++) {
@@ -78,7 +78,7 @@ __device__ __forceinline__ void quant_step(const v4i (&x)[4], int rw0, int rows,
     o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[1]), s, 1);
     o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[2]), s, 2);
     o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[3]), s, 3);
-    if (ok) *(uint32_t*)(cptr[q] + 32 * st) = o;
+    if (ok) store(q, st, o);
     // scale bytes of (row, blocks 2st, 2st+1): the row's first lane takes the
     // second quad's code along (row_shl:4) and writes both
     const uint32_t code2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)code, 0x104, 0xF, 0xF, true);
@@ -162,6 +162,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
   uint8_t* cptr[4];
 #pragma unroll
   for (int q = 0; q < 4; q++) cptr[q] = codes + (size_t)(rw0 + 8 * q + lr) * (cols >> 1) + ((c0 + lc) >> 1);
+  auto store = [&](int q, int st, uint32_t o) { *(uint32_t*)(cptr[q] + 32 * st) = o; };
 
 #pragma unroll
   for (int st = 0; st < NST; st++) {
@@ -172,9 +173,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
     // interior (every row of the wave and both blocks of the step in range):
     // no masking; the edge path zeroes what lies outside
     if (rw0 + 32 > rows || 2 * st + 2 > nblk)
-      quant_step<true, MODE != 0>(xv[st], rw0, rows, col_ok, lr, lc, lane, cptr, st, sc, L::SC_ROW, xt);
+      quant_step<true, MODE != 0>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt);
     else
-      quant_step<false, MODE != 0>(xv[st], rw0, rows, col_ok, lr, lc, lane, cptr, st, sc, L::SC_ROW, xt);
+      quant_step<false, MODE != 0>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt);
 
     if constexpr (MODE != 0) {
       const int g16 = lane >> 4, t16 = lane & 15;
@@ -241,6 +242,173 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
   }
 }
 
+// ---------------------------------------------------------------- full rows
+// Projection [cols, R] only.  Workgroup = WAVES waves over 32 whole rows;
+// wave w takes the 64-column steps w, w + WAVES, ...  A step is handled as in
+// k_quant_rows: row-contiguous loads (every 8 lanes read one 128-byte line),
+// block scales and codes from lane quads, the bf16 values through a private
+// LDS tile into the MFMA layout.  The step's 64 projection rows come with it,
+// also as whole 128-byte lines, into a second private tile that is read back
+// transposed.  The waves' partial projections are added in LDS in wave
+// order: nothing partial leaves the workgroup and no reduction kernel
+// follows.  The price is one read of the projection matrix (from L2) per 32
+// rows, on fewer workgroups than the chunked kernel has.
+constexpr int QF_MAX_BLOCKS = 512;   // scale bytes per row staged in LDS: cols <= 16384
+
+template <int RT, int WAVES>
+struct QuantFrLds {
+  static constexpr int PSTRIDE = RT * 32 + 16;                        // projection tile [64 k][RT*32] (halfwords)
+  static constexpr int PTILE = 64 * PSTRIDE * 2;
+  static constexpr int XTILE = 32 * QR_XSTRIDE * 2;
+  static constexpr int WAVE_BYTES = PTILE + XTILE;
+  static constexpr int RED = WAVES * RT * 16 * 64 * 4;               // the waves' accumulators
+  static constexpr int WORK = WAVES * WAVE_BYTES > RED ? WAVES * WAVE_BYTES : RED;
+  static constexpr int BYTES = WORK + 32 * QF_MAX_BLOCKS;
+};
+
+template <int RT, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __restrict__ src, int rows, int cols,
+                                                              uint8_t* __restrict__ codes,
+                                                              uint8_t* __restrict__ scales,
+                                                              const uint16_t* __restrict__ proj, int R,
+                                                              float* __restrict__ proj_out) {
+  using L = QuantFrLds<RT, WAVES>;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[L::BYTES];
+  constexpr int NT = 64 * WAVES;
+  constexpr int NP = 4 * RT;        // 16-byte projection loads per lane and step
+  constexpr int NB = 3;             // step buffers: two steps in flight ahead of the one consumed
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int row0 = blockIdx.x * 32;
+  const int lr = lane >> 3, lc = (lane & 7) * 8;     // row within an 8-row group, column within a step
+  const int nsteps = (cols + 63) >> 6;
+  const int nmine = wave < nsteps ? (nsteps - 1 - wave) / WAVES + 1 : 0;
+  const int nbc = cols >> 5;
+  FT_LDS uint8_t* sc = (FT_LDS uint8_t*)(lds + L::WORK);             // [32 rows][QF_MAX_BLOCKS] scale bytes
+  FT_LDS uint16_t* pt = (FT_LDS uint16_t*)(lds + wave * L::WAVE_BYTES);   // projection tile
+  FT_LDS uint16_t* xt = (FT_LDS uint16_t*)(lds + wave * L::WAVE_BYTES + L::PTILE);   // bf16 tile [32][64]
+  // Buffer offsets: per lane and constant over the steps (rows past the
+  // matrix and projection columns past R get an out-of-range offset and
+  // read zeros; projection rows past cols lie past the buffer), plus a
+  // uniform offset per step.
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(src, (uint32_t)((size_t)rows * cols * 2));
+  const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes, (uint32_t)((size_t)rows * cols / 2));
+  const __amdgpu_buffer_rsrc_t rp = make_rsrc(proj, (uint32_t)((size_t)R * cols * 2));
+  uint32_t xoff[4], coff[4], poff[NP];
+#pragma unroll
+  for (int q = 0; q < 4; q++) {
+    const int r = row0 + 8 * q + lr;
+    xoff[q] = r < rows ? (uint32_t)(r * cols + lc) * 2u : kOobOffset;
+    coff[q] = r < rows ? (uint32_t)(r * (cols >> 1) + (lc >> 1)) : kOobOffset;
+  }
+#pragma unroll
+  for (int q = 0; q < NP; q++) {   // 16-byte slot lane + 64q of the step's [64 k][RT*32] rows
+    const int sl = lane + 64 * q, kr = sl / (RT * 4), c16 = sl % (RT * 4);
+    poff[q] = 8 * c16 < R ? (uint32_t)(kr * R + 8 * c16) * 2u : kOobOffset;
+  }
+  auto store = [&](int q, int st, uint32_t o) {
+    __builtin_amdgcn_raw_buffer_store_b32(o, rc, coff[q], 32 * st, 0);
+  };
+
+  auto step_of = [&](int k) { return wave + k * WAVES; };
+
+  struct Ops { v4i x[4]; v4i p[NP]; };
+  // Loads of local step k.  On the last step of a row whose length is an odd
+  // multiple of 32, the upper lanes read past the row; quant_step zeroes those
+  // values (the projection rows there lie past the buffer).
+  auto issue = [&](int k, Ops& o) {
+    const int c = 64 * step_of(k);
+#pragma unroll
+    for (int q = 0; q < 4; q++) o.x[q] = __builtin_amdgcn_raw_buffer_load_b128(rx, xoff[q], 2 * c, 0);
+#pragma unroll
+    for (int q = 0; q < NP; q++)
+      o.p[q] = __builtin_amdgcn_raw_buffer_load_b128(rp, poff[q], 2 * c * R, 0);
+  };
+
+  v16f acc[RT];
+#pragma unroll
+  for (int t = 0; t < RT; t++) acc[t] = v16f{};
+  const int r32 = lane & 31, h = lane >> 5, g16 = lane >> 4, t16 = lane & 15;
+
+  auto consume = [&](int k, Ops& o) {
+    const int st = step_of(k), c = 64 * st;
+    const int blk = 2 * st + (lane >> 2 & 1);
+    const bool col_ok = blk < nbc;
+    if (row0 + 32 > rows || c + 64 > cols)
+      quant_step<true, true>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt);
+    else
+      quant_step<false, true>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt);
+    // the step's projection rows
+#pragma unroll
+    for (int q = 0; q < NP; q++) {
+      const int sl = lane + 64 * q, kr = sl / (RT * 4), c16 = sl % (RT * 4);
+      *(FT_LDS v4i*)(pt + kr * L::PSTRIDE + 8 * c16) = o.p[q];
+    }
+#pragma unroll
+    for (int kk = 0; kk < 4; kk++) {
+      const v8bf a = __builtin_bit_cast(v8bf, *(const FT_LDS v4i*)(xt + r32 * QR_XSTRIDE + 16 * kk + 8 * h));
+#pragma unroll
+      for (int t = 0; t < RT; t++) {
+        // group g16 covers columns t*32 + 16(g16 & 1) + [0,16), reduction rows 16kk + 8h + [0,8)
+        const int jj = t16 >> 2, qq = t16 & 3;
+        const FT_LDS uint16_t* base = pt + (16 * kk + 8 * h + jj) * L::PSTRIDE + t * 32 + 16 * (g16 & 1) + 4 * qq;
+        const v8bf b = make_v8bf(lds_read_tr16((const FT_LDS void*)base),
+                                 lds_read_tr16((const FT_LDS void*)(base + 4 * L::PSTRIDE)));
+        acc[t] = mfma_bf16_32x32x16(a, b, acc[t]);
+      }
+    }
+  };
+
+  Ops buf[NB];
+#pragma unroll
+  for (int k = 0; k < NB - 1; k++)
+    if (k < nmine) issue(k, buf[k]);
+#pragma unroll 1
+  for (int k0 = 0; k0 < nmine; k0 += NB) {
+#pragma unroll
+    for (int u = 0; u < NB; u++) {
+      const int k = k0 + u;
+      if (k < nmine) {
+        if (k + NB - 1 < nmine) issue(k + NB - 1, buf[(u + NB - 1) % NB]);
+        consume(k, buf[u]);
+      }
+    }
+  }
+
+  // the waves' partial projections, added in wave order
+  __syncthreads();
+  float* red = (float*)lds;
+#pragma unroll
+  for (int t = 0; t < RT; t++)
+#pragma unroll
+    for (int v = 0; v < 16; v++) red[((wave * RT + t) * 16 + v) * 64 + lane] = acc[t][v];
+  __syncthreads();
+  constexpr int NOUT = RT * 16 * 64;
+  for (int o = tid; o < NOUT; o += NT) {
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < WAVES; w++) sum += red[w * NOUT + o];
+    const int t = o >> 10, v = (o >> 6) & 15, ln = o & 63;
+    const int r = row0 + 8 * (v >> 2) + 4 * (ln >> 5) + (v & 3), j = t * 32 + (ln & 31);
+    if (r < rows && j < R) proj_out[(size_t)r * R + j] = sum;
+  }
+  // scale bytes of the workgroup's rows
+  const int nw = (nbc + 3) >> 2;
+  const bool al = (nbc & 3) == 0;
+  for (int d = tid; d < 32 * nw; d += NT) {
+    const int rr = d / nw, dw = d % nw, r = row0 + rr;
+    if (r >= rows) continue;
+    uint8_t* dst = scales + (size_t)r * nbc + 4 * dw;
+    const FT_LDS uint8_t* sp = sc + rr * QF_MAX_BLOCKS + 4 * dw;
+    if (al) {
+      *(uint32_t*)dst = *(const FT_LDS uint32_t*)sp;
+    } else {
+      for (int b = 0; b < 4 && 4 * dw + b < nbc; b++) dst[b] = sp[b];
+    }
+  }
+}
+
 // ---------------------------------------------------------------- tiles
 // One wave per 32x32 tile: lane l takes row l/2, columns 16*(l%2) + [0,16).
 __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict__ src, int rows, int cols,
@@ -292,8 +460,18 @@ static int quant_chunk_cols(int rows, int cols, int R, int layout) {
   return (R + 31) / 32 <= 2 ? 768 : 384;
 }
 
+// Whole rows per workgroup (no partial sums) for proj [cols, R] when 32-row
+// workgroups make between 64 and one round of 256 and the projection is at
+// most 64 wide (4608 x 3072: 15.6 us against 18 with the chunks' reduction).
+// For proj [R, cols] at 4608 x 9216 the chunked kernel is faster (33 against
+// 36 us): the step work of 4608 rows on 144 workgroups outweighs the partial sums.
+static bool quant_full_rows(int rows, int cols, int R, int layout) {
+  const int wg = (rows + 31) / 32;
+  return layout == 0 && R > 0 && R <= 64 && cols <= 32 * QF_MAX_BLOCKS && wg >= 64 && wg <= 256;
+}
+
 size_t quant_rows_workspace(int rows, int cols, int R, int layout) {
-  if (R == 0) return 0;
+  if (R == 0 || quant_full_rows(rows, cols, R, layout)) return 0;
   const int cw = quant_chunk_cols(rows, cols, R, layout);
   const int chunks = (cols + cw - 1) / cw;
   return chunks > 1 ? (size_t)chunks * rows * R * sizeof(float) : 0;
@@ -315,6 +493,12 @@ hipError_t launch_quant_rows(const uint16_t* src, int rows, int cols, uint8_t* c
   if (!proj || R == 0)
     return launch_rows_t<1, 0, 4, 384>(src, rows, cols, codes, scales, nullptr, 0, nullptr, nullptr, st);
   const int rt = (R + 31) / 32;
+  if (quant_full_rows(rows, cols, R, layout)) {
+    const unsigned grid = (unsigned)((rows + 31) / 32);
+    if (rt == 1) k_quant_rows_fr<1, 8><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out);
+    else k_quant_rows_fr<2, 8><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out);
+    return hipGetLastError();
+  }
   if (layout == 0) {
     if (quant_chunk_cols(rows, cols, R, layout) == 256) {
       switch (rt) {

@@ -79,14 +79,19 @@ def test_quantize_validation():
     # empty input is a no-op, even with NULL buffers
     assert q(NULL, 0, 64, 1, NULL, NULL) == _lib.FT_OK
     # a projection over several column chunks needs the workspace the size query reports
-    need = _lib.ft_quantize_workspace_size(4608, 3072, 1, 64, 0)
-    assert need == 12 * 4608 * 64 * 4      # 256-column chunks: 384 would leave fewer workgroups than CUs
-    assert _lib.ft_quantize_workspace_size(18432, 15360, 1, 96, 0) == 40 * 18432 * 96 * 4   # 384 otherwise
-    assert _lib.ft_quantize_workspace_size(4608, 9216, 1, 64, 1) == 12 * 4608 * 64 * 4   # 768 for [R, cols]
-    assert _lib.ft_quantize_workspace_size(4608, 256, 1, 64, 0) == 0                     # one chunk: none
+    need = _lib.ft_quantize_workspace_size(512, 3072, 1, 64, 0)
+    assert need == 12 * 512 * 64 * 4       # 256-column chunks: 384 would leave fewer workgroups than CUs
+    assert _lib.ft_quantize_workspace_size(8224, 3072, 1, 64, 0) == 8 * 8224 * 64 * 4     # 384 otherwise
+    assert _lib.ft_quantize_workspace_size(18432, 15360, 1, 96, 0) == 40 * 18432 * 96 * 4
+    assert _lib.ft_quantize_workspace_size(512, 9216, 1, 64, 1) == 12 * 512 * 64 * 4     # 768 for [R, cols]
+    assert _lib.ft_quantize_workspace_size(512, 256, 1, 64, 0) == 0                      # one chunk: none
+    # whole rows per workgroup for [cols, R] (64..256 workgroups of 32 rows, R <= 64): no partial sums
+    assert _lib.ft_quantize_workspace_size(4608, 3072, 1, 64, 0) == 0
+    assert _lib.ft_quantize_workspace_size(4608, 9216, 1, 64, 1) == 12 * 4608 * 64 * 4   # [R, cols]: chunks
+    assert _lib.ft_quantize_workspace_size(4608, 3072, 1, 96, 0) > 0                     # R > 64: chunks
     assert _lib.ft_quantize_workspace_size(4608, 3072, 1, 0, 0) == 0                     # no projection: none
     assert _lib.ft_quantize_workspace_size(4608, 3072, 32, 0, 0) == 0
-    big = (ALIGNED, 4608, 3072, 1, ALIGNED, ALIGNED, ALIGNED2, 64, 0, ALIGNED2)
+    big = (ALIGNED, 512, 3072, 1, ALIGNED, ALIGNED, ALIGNED2, 64, 0, ALIGNED2)
     assert q(*big) == _lib.FT_ERR_NULL
     assert q(*big, ws=ALIGNED2, wsb=need - 16) == _lib.FT_ERR_SHAPE
     assert q(*big, ws=MISALIGNED, wsb=need) == _lib.FT_ERR_ALIGN
