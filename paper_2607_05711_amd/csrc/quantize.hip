@@ -253,7 +253,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
 // order: nothing partial leaves the workgroup and no reduction kernel
 // follows.  The price is one read of the projection matrix (from L2) per 32
 // rows, on fewer workgroups than the chunked kernel has.
-constexpr int QF_MAX_BLOCKS = 512;   // scale bytes per row staged in LDS: cols <= 16384
+constexpr int QF_MAX_BLOCKS = 128;   // scale bytes per row staged in LDS: cols <= 4096
 
 template <int RT, int WAVES>
 struct QuantFrLds {
@@ -461,10 +461,12 @@ static int quant_chunk_cols(int rows, int cols, int R, int layout) {
 }
 
 // Whole rows per workgroup (no partial sums) for proj [cols, R] when 32-row
-// workgroups make between 64 and one round of 256 and the projection is at
-// most 64 wide (4608 x 3072: 15.6 us against 18 with the chunks' reduction).
-// For proj [R, cols] at 4608 x 9216 the chunked kernel is faster (33 against
-// 36 us): the step work of 4608 rows on 144 workgroups outweighs the partial sums.
+// workgroups make between 64 and one round of 256, rows are at most 4096
+// long and the projection is at most 64 wide (4608 x 3072: 16.5 us against
+// 17.8 with the chunks' reduction).  Longer rows make each workgroup read a
+// larger projection matrix (4608 x 15360: 94 us against 80).  For proj
+// [R, cols] at 4608 x 9216 the chunked kernel is faster (33 against 36 us):
+// the step work of 4608 rows on 144 workgroups outweighs the partial sums.
 static bool quant_full_rows(int rows, int cols, int R, int layout) {
   const int wg = (rows + 31) / 32;
   return layout == 0 && R > 0 && R <= 64 && cols <= 32 * QF_MAX_BLOCKS && wg >= 64 && wg <= 256;

@@ -87,6 +87,7 @@ def test_quantize_validation():
     assert _lib.ft_quantize_workspace_size(512, 256, 1, 64, 0) == 0                      # one chunk: none
     # whole rows per workgroup for [cols, R] (64..256 workgroups of 32 rows, R <= 64): no partial sums
     assert _lib.ft_quantize_workspace_size(4608, 3072, 1, 64, 0) == 0
+    assert _lib.ft_quantize_workspace_size(4608, 15360, 1, 64, 0) > 0                    # rows > 4096: chunks
     assert _lib.ft_quantize_workspace_size(4608, 9216, 1, 64, 1) == 12 * 4608 * 64 * 4   # [R, cols]: chunks
     assert _lib.ft_quantize_workspace_size(4608, 3072, 1, 96, 0) > 0                     # R > 64: chunks
     assert _lib.ft_quantize_workspace_size(4608, 3072, 1, 0, 0) == 0                     # no projection: none
