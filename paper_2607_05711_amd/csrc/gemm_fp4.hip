@@ -1011,21 +1011,26 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     const __amdgpu_buffer_rsrc_t r_q = make_rsrc(ep.q, (uint32_t)M * (NO / 2));
     const int g16 = lane >> 4, t16 = lane & 15, jj = t16 >> 2, qq = t16 & 3;
     const int rt2 = (R2 + 31) >> 5;
-    // EPI_DGELU: every z segment this lane needs, loaded before the first
-    // store (a load waited for after stores would wait for those stores too)
-    v4i zpre[4][8];
-    if constexpr (!G) {
+    // EPI_DGELU: the z segments of pass i are loaded at the start of pass
+    // i - 1, ahead of that pass's stores, so that waiting for them waits
+    // only for the stores of pass i - 2 (loads and stores retire in order).
+    // Issuing all passes' loads at once made every CU load its whole z tile
+    // in one burst at the start of the epilogue.
+    v4i zpre[2][8];
+    auto load_z = [&](int i, v4i (&zd)[8]) {
 #pragma unroll
-      for (int i = 0; i < 4; i++)
-#pragma unroll
-        for (int it = 0; it < 8; it++) {
-          const int gr = orow0 + 32 * i + 4 * it + g16, gc = ocol0 + 8 * t16;
-          zpre[i][it] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
-              r_z, (gr < M && gc < NO) ? ((uint32_t)gr * NO + gc) * 2 : kOobOffset, 0, 0));
-        }
-    }
+      for (int it = 0; it < 8; it++) {
+        const int gr = orow0 + 32 * i + 4 * it + g16, gc = ocol0 + 8 * t16;
+        zd[it] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+            r_z, (gr < M && gc < NO) ? ((uint32_t)gr * NO + gc) * 2 : kOobOffset, 0, 0));
+      }
+    };
+    if constexpr (!G) load_z(0, zpre[0]);
 #pragma unroll   // acc[i] must be indexed by constants
     for (int i = 0; i < 4; i++) {
+      if constexpr (!G) {
+        if (i + 1 < 4) load_z(i + 1, zpre[(i + 1) & 1]);
+      }
       // 1) stage this pass's 32 rows
 #pragma unroll
       for (int j = 0; j < 4; j++)
@@ -1044,9 +1049,6 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
           }
         }
       __builtin_amdgcn_s_waitcnt(0xc07f);
-      if constexpr (!G) {
-        if (i == 0) wait_vm<0>();   // z arrived (no store issued yet)
-      }
       // 2) row segments: outputs, block codes, bf16 result back in place
 #pragma unroll
       for (int it = 0; it < 8; it++) {
@@ -1066,7 +1068,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
           }
         } else {
           const float4 d0 = *(const float4*)(srow + seg * 32), d1 = *(const float4*)(srow + seg * 32 + 16);
-          const v4i zb = zpre[i][it];
+          const v4i zb = zpre[i & 1][it];
           const float dh[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
 #pragma unroll
           for (int e = 0; e < 4; e++) {
