@@ -4,6 +4,10 @@
 // gradients G, FourTune Sec. 3.1 dynamic quantization), fused with the
 // low-rank down-projection of the same rows (Sec. 3.3, LoRA fusion: the
 // stabilizer and adapter branches share the input, so one pass reads it once).
+// Workgroups cover column chunks; their partial projections are summed by
+// k_reduce_parts.
+// k_quant_rows_fr: the same for a [cols, R] projection with whole rows per
+// workgroup, which adds its partial projections itself.
 // k_quant_tiles: 32x32 tiles of the frozen weight (Sec. 3.2), offline.
 #include "ft_device.h"
 #include "ft_kernels.h"
