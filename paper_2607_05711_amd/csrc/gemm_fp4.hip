@@ -333,18 +333,6 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   // Accumulator tiles are computed transposed (W fragment as MFMA operand A):
   // lane (r32, h) of tile acc[i][j] holds output row wm*128 + 32i + r32 and,
   // in element 4q + e, column wn*128 + 32j + 8q + 4h + e.
-  // Bias of this lane's columns (forward): four bf16 per (j, q), loaded first.
-  uint2 bias4[4][4];
-#pragma unroll
-  for (int j = 0; j < 4; j++)
-#pragma unroll
-    for (int q = 0; q < 4; q++) {
-      bias4[j][q] = make_uint2(0u, 0u);
-      if constexpr (!BWD) {
-        const int gc = n0 + wn * 128 + j * 32 + 8 * q + 4 * h;
-        if (bias && gc < N) bias4[j][q] = *(const uint2*)(bias + gc);
-      }
-    }
 
   // ---------------- per-lane load geometry (constant over stages)
   // Each buffer load takes a per-lane byte offset (rows outside the matrix
@@ -711,6 +699,24 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
   // of stage 1 start here.
   issue_part1(0);
   issue_part2(0);
+  // Bias of this lane's columns (forward): four bf16 per (j, q), loaded
+  // behind stage 0 so that the two latencies overlap.  Buffer loads without
+  // branches: columns past N (and a missing bias, an empty buffer) read zeros.
+  uint2 bias4[4][4];
+  {
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(bias, bias ? (uint32_t)N * 2 : 0u);
+#pragma unroll
+    for (int j = 0; j < 4; j++)
+#pragma unroll
+      for (int q = 0; q < 4; q++) {
+        bias4[j][q] = make_uint2(0u, 0u);
+        if constexpr (!BWD) {
+          const int gc = n0 + wn * 128 + j * 32 + 8 * q + 4 * h;
+          const v2i b = __builtin_amdgcn_raw_buffer_load_b64(rb, gc < N ? (uint32_t)gc * 2 : kOobOffset, 0, 0);
+          bias4[j][q] = make_uint2((uint32_t)b[0], (uint32_t)b[1]);
+        }
+      }
+  }
   if (1 < total) {
     if (1 < nst) {
       const bool hf = half_last && 1 == nst - 1;
