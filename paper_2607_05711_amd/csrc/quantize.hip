@@ -231,16 +231,23 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
   }
 
   if constexpr (MODE != 0) {
-    // this chunk's partial (several chunks) or the projection itself (one chunk)
+    // this chunk's partial (several chunks) or the projection itself (one
+    // chunk), one 32-column tile at a time through the wave's own bf16 tile
+    // (32 rows x 36 fp32 fit its 32 x 72 halfwords), stored as row-contiguous
+    // 16-byte runs: 4 stores per tile instead of 16
+    static_assert(32 * 36 * 4 == L::X_HW * 2, "fp32 tile in the bf16 tile's place");
     float* dst = parts ? parts + (size_t)blockIdx.y * rows * R : proj_out;
+    FT_LDS float* pst = (FT_LDS float*)xt;
 #pragma unroll
     for (int t = 0; t < RT; t++) {
-      const int j = t * 32 + r32;
-      if (j >= R) continue;
 #pragma unroll
-      for (int v = 0; v < 16; v++) {
-        const int rr = rw0 + 8 * (v >> 2) + 4 * h + (v & 3);
-        if (rr < rows) dst[(size_t)rr * R + j] = acc[t][v];
+      for (int v = 0; v < 16; v++) pst[(8 * (v >> 2) + 4 * h + (v & 3)) * 36 + r32] = acc[t][v];
+#pragma unroll
+      for (int q = 0; q < 4; q++) {
+        const int idx = lane + 64 * q, row = idx >> 3, c4 = idx & 7;
+        const v4i val = *(const FT_LDS v4i*)(pst + row * 36 + 4 * c4);   // four fp32, copied as bits
+        const int rr = rw0 + row, j = t * 32 + 4 * c4;
+        if (rr < rows && j < R) *(v4i*)(dst + (size_t)rr * R + j) = val;
       }
     }
   }
