@@ -106,7 +106,7 @@ def test_quantize_tiles_bitexact(rows, cols):
                                                 # fewer steps than waves, projections narrower than their
                                                 # 32-column tiles
                                                 (2304, 4064, 64, 0), (2200, 1056, 16, 0), (2100, 160, 64, 0),
-                                                (8192, 800, 48, 0),
+                                                (8192, 800, 48, 0), (2080, 96, 32, 0),
                                                 # [R, cols] at the same row counts (column chunks)
                                                 (2065, 4160, 64, 1), (3000, 2080, 32, 1), (2080, 640, 48, 1)])
 def test_quantize_fused_projection(rows, cols, R, layout):
