@@ -397,6 +397,32 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = t0.elapsed_time(t1) / args.steps
 
+    # per-step times: warm (back to back) and with the caches flushed before
+    # every step by reading a 1 GiB buffer (L2 and the 256 MB last-level
+    # cache then hold that buffer's clean lines, not the step's inputs)
+    nps = min(args.steps, 20)
+    flush_buf = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+
+    def per_step(flush):
+        evs_ = []
+        for _ in range(nps):
+            if flush:
+                flush_buf.sum(dtype=torch.int64)
+            a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a_.record()
+            step_timed()
+            b_.record()
+            evs_.append((a_, b_))
+        torch.cuda.synchronize()
+        return sorted(a_.elapsed_time(b_) for a_, b_ in evs_)
+
+    def summary(v):
+        q = lambda p: v[min(len(v) - 1, int(round(p * (len(v) - 1))))]
+        return {"median": round(q(0.5), 4), "p10": round(q(0.1), 4), "p90": round(q(0.9), 4)}
+
+    step_warm, step_flushed = summary(per_step(False)), summary(per_step(True))
+    del flush_buf
+
     # per-kernel timing: events around each call, same stream (a few steps)
     psteps = min(args.steps, 20 if len(ops) < 50 else 2)
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)] for _ in range(psteps)]
@@ -457,6 +483,9 @@ def main():
                      "traffic": measured_traffic("bwd" if gemm == "gemm_bwd" else "fwd")
                      if args.workload == "flux_qkv" else None,
                      "per_launch_flops": per_call_flops, "avg_launch_us": round(launch_us[gemm], 2)},
+        "step_ms": {"steps": nps, "warm": step_warm, "flushed": step_flushed,
+                    "flush": "1 GiB read before each step (L2 and last-level cache hold no inputs)",
+                    "flushed_tflops_median": round(counts["flops"] / (step_flushed["median"] * 1e-3) / 1e12, 2)},
         "kernels_us": {k: round(step_us[k], 2) for k in kinds},
         "kernels_frac": frac,
     }
