@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="token rows in the oracle sample (0: auto)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="flux_qkv / flux_mlp: time the fused step against an unfused one, print one JSON line, exit")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (scales HBM counters), then exit")
     return ap.parse_args()
@@ -295,6 +297,156 @@ class Builder:
         return fwd, bwd, counts
 
 
+def fusion_ablation(torch, L, d, wq, ws, shape, steps, warmup):
+    """The layer step with and without the low-rank fusion (the paper's LoRA
+    fusion, Sec. 3.3), same inputs.  Unfused: quantization without the
+    projection, the FP4 GEMMs without the low-rank branch, and the low-rank
+    down- and up-projections and adapter gradients as separate bf16 library
+    matmuls (each re-reading its [M, K] or [M, N] operand).  A timing
+    comparison only: the unfused step keeps its low-rank intermediates in
+    bf16."""
+    M, K, N, r, rs = shape.M, shape.K, shape.N, shape.r, shape.r_s
+    R = r + rs
+    dev = d["X"].device
+    X, dY, D, U, bias = d["X"], d["dY"], d["D"], d["U"], d["bias"]
+    u8, f32, bf = torch.uint8, torch.float32, torch.bfloat16
+    e = lambda sh, t: torch.empty(sh, dtype=t, device=dev)
+    xq, xs, gq, gs = e((M, K // 2), u8), e((M, K // 32), u8), e((M, N // 2), u8), e((M, N // 32), u8)
+    P, Qp = e((M, R), f32), e((M, R), f32)
+    Y, dX = e((M, N), bf), e((M, K), bf)
+    dA, dB = e((K, r), f32), e((r, N), f32)
+    wx = e((max(16, L.ft_quantize_workspace_size(M, K, 1, R, L.FT_PROJ_COLS_BY_R)),), u8)
+    wd = e((max(16, L.ft_quantize_workspace_size(M, N, 1, R, L.FT_PROJ_R_BY_COLS)),), u8)
+    wl = e((max(16, L.ft_lora_grads_workspace_size(M, K, N, R, r)),), u8)
+    Ut, Dt = U.t().contiguous(), D.t().contiguous()       # [N, R], [R, K]: contiguous matmul operands
+    dBb, dAtb = e((r, N), bf), e((r, K), bf)
+
+    def fused():
+        L.ft_quantize_blockwise(X, proj=D, codes=xq, scales=xs, proj_out=P, workspace=wx)
+        L.ft_linear_fwd(xq, xs, wq, ws, K, P, U, bias, y=Y)
+        L.ft_quantize_blockwise(dY, proj=U, proj_layout=L.FT_PROJ_R_BY_COLS, codes=gq, scales=gs, proj_out=Qp,
+                                workspace=wd)
+        L.ft_linear_bwd_input(gq, gs, wq, ws, K, Qp, D, dx=dX)
+        L.ft_lora_grads(X, dY, P, Qp, r, col0=rs, dA=dA, dB=dB, workspace=wl)
+
+    def unfused():
+        L.ft_quantize_blockwise(X, codes=xq, scales=xs)
+        Pb = torch.mm(X, D)                                   # [M, R] bf16, re-reads X
+        L.ft_linear_fwd(xq, xs, wq, ws, K, None, None, bias, y=Y)
+        Y.add_(torch.mm(Pb, U))                               # up-projection, then a pass over Y
+        L.ft_quantize_blockwise(dY, codes=gq, scales=gs)
+        Qb = torch.mm(dY, Ut)                                 # [M, R], re-reads dY
+        L.ft_linear_bwd_input(gq, gs, wq, ws, K, dx=dX)
+        dX.add_(torch.mm(Qb, Dt))
+        torch.mm(Pb[:, rs:].t().contiguous(), dY, out=dBb)   # dB = (XA)^T dY
+        torch.mm(Qb[:, rs:].t().contiguous(), X, out=dAtb)   # dA^T = (dY B^T)^T X
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    tf, tu = timed(fused), timed(unfused)
+    tf2 = timed(fused)
+    tf = min(tf, tf2)
+    return {"metric": "layer step time, low-rank fusion ablation (flux_qkv)", "unit": "ms",
+            "fused_ms": round(tf, 4), "unfused_ms": round(tu, 4), "fusion_speedup": round(tu / tf, 3),
+            "unfused": "quantize without projection; FP4 GEMMs without the low-rank branch; down-, up-projections "
+                       "and adapter gradients as separate bf16 library matmuls",
+            "steps": steps, "warmup": warmup, "data": "synthetic"}
+
+
+def mlp_ablation(torch, L, dev, seed, steps, warmup, M=4608, Dm=3072, F=12288, r=32, rs=32):
+    """The MLP pair step with and without the MLP fusion (Sec. 3.3): the
+    fused step runs FC1 with the GELU / quantize / projection epilogue and
+    FC2's backward-input with the dGELU epilogue; the unfused step writes z
+    and dH from plain GEMMs and applies GELU-tanh and its derivative as
+    library elementwise kernels before quantizing h and dz with their
+    projections.  Both keep the low-rank fusion.  A timing comparison only."""
+    t, R = torch, r + rs
+    g = t.Generator(device=dev)
+    g.manual_seed(seed)
+    u8, f32, bf = t.uint8, t.float32, t.bfloat16
+    e = lambda sh, dt: t.empty(sh, dtype=dt, device=dev)
+    nrm = lambda sh, sd: (t.randn(sh, generator=g, device=dev) * sd).to(bf)
+    X, dY = nrm((M, Dm), 1.0), nrm((M, Dm), 1e-3)
+    w1q, w1s, _ = L.ft_quantize_blockwise(nrm((F, Dm), 0.02), block_rows=32)
+    w2q, w2s, _ = L.ft_quantize_blockwise(nrm((Dm, F), 0.02), block_rows=32)
+    D1, U1, b1 = nrm((Dm, R), 0.01), nrm((R, F), 0.01), nrm((F,), 0.02)
+    D2, U2, b2 = nrm((F, R), 0.01), nrm((R, Dm), 0.01), nrm((Dm,), 0.02)
+    xq, xs = e((M, Dm // 2), u8), e((M, Dm // 32), u8)
+    P1, P2, Qp1, Qp2 = (e((M, R), f32) for _ in range(4))
+    z, h, dz, dH = (e((M, F), bf) for _ in range(4))
+    hq, hs, dzq, dzs = e((M, F // 2), u8), e((M, F // 32), u8), e((M, F // 2), u8), e((M, F // 32), u8)
+    Y, dX = e((M, Dm), bf), e((M, Dm), bf)
+    gq, gs = e((M, Dm // 2), u8), e((M, Dm // 32), u8)
+    dA1, dB1, dA2, dB2 = e((Dm, r), f32), e((r, F), f32), e((F, r), f32), e((r, Dm), f32)
+    ws = lambda n: e((max(16, n),), u8)
+    wx = ws(L.ft_quantize_workspace_size(M, Dm, 1, R, L.FT_PROJ_COLS_BY_R))
+    wd = ws(L.ft_quantize_workspace_size(M, Dm, 1, R, L.FT_PROJ_R_BY_COLS))
+    wh = ws(L.ft_quantize_workspace_size(M, F, 1, R, L.FT_PROJ_COLS_BY_R))
+    wz = ws(L.ft_quantize_workspace_size(M, F, 1, R, L.FT_PROJ_R_BY_COLS))
+    wg = ws(L.ft_linear_fwd_gelu_workspace_size(M, F, R))
+    wdg = ws(L.ft_linear_bwd_input_dgelu_workspace_size(M, F, R))
+    wl1, wl2 = ws(L.ft_lora_grads_workspace_size(M, Dm, F, R, r)), ws(L.ft_lora_grads_workspace_size(M, F, Dm, R, r))
+
+    def common_tail():
+        L.ft_linear_bwd_input(dzq, dzs, w1q, w1s, Dm, Qp1, D1, dx=dX)
+        L.ft_lora_grads(h, dY, P2, Qp2, r, col0=rs, dA=dA2, dB=dB2, workspace=wl2)
+        L.ft_lora_grads(X, dz, P1, Qp1, r, col0=rs, dA=dA1, dB=dB1, workspace=wl1)
+
+    def fused():
+        L.ft_quantize_blockwise(X, proj=D1, codes=xq, scales=xs, proj_out=P1, workspace=wx)
+        L.ft_linear_fwd_gelu(xq, xs, w1q, w1s, Dm, P1, U1, b1, D2=D2, z=z, h=h, hq=hq, hs=hs, P2=P2, workspace=wg)
+        L.ft_linear_fwd(hq, hs, w2q, w2s, F, P2, U2, b2, y=Y)
+        L.ft_quantize_blockwise(dY, proj=U2, proj_layout=L.FT_PROJ_R_BY_COLS, codes=gq, scales=gs, proj_out=Qp2,
+                                workspace=wd)
+        L.ft_linear_bwd_input_dgelu(gq, gs, w2q, w2s, F, z, Qp2, D2, U1=U1, dz=dz, dzq=dzq, dzs=dzs, Qp1=Qp1,
+                                    workspace=wdg)
+        common_tail()
+
+    def unfused():
+        L.ft_quantize_blockwise(X, proj=D1, codes=xq, scales=xs, proj_out=P1, workspace=wx)
+        L.ft_linear_fwd(xq, xs, w1q, w1s, Dm, P1, U1, b1, y=z)
+        t.ops.aten.gelu.out(z, approximate="tanh", out=h)
+        L.ft_quantize_blockwise(h, proj=D2, codes=hq, scales=hs, proj_out=P2, workspace=wh)
+        L.ft_linear_fwd(hq, hs, w2q, w2s, F, P2, U2, b2, y=Y)
+        L.ft_quantize_blockwise(dY, proj=U2, proj_layout=L.FT_PROJ_R_BY_COLS, codes=gq, scales=gs, proj_out=Qp2,
+                                workspace=wd)
+        L.ft_linear_bwd_input(gq, gs, w2q, w2s, F, Qp2, D2, dx=dH)
+        t.ops.aten.gelu_backward.grad_input(dH, z, approximate="tanh", grad_input=dz)
+        L.ft_quantize_blockwise(dz, proj=U1, proj_layout=L.FT_PROJ_R_BY_COLS, codes=dzq, scales=dzs, proj_out=Qp1,
+                                workspace=wz)
+        common_tail()
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        t.cuda.synchronize()
+        a, b = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        t.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    tf, tu = timed(fused), timed(unfused)
+    tf = min(tf, timed(fused))
+    return {"metric": "MLP pair step time, MLP fusion ablation (flux_mlp)", "unit": "ms",
+            "fused_ms": round(tf, 4), "unfused_ms": round(tu, 4), "fusion_speedup": round(tu / tf, 3),
+            "unfused": "FC1 and FC2 backward-input as plain GEMMs writing z and dH; GELU-tanh and its derivative "
+                       "as library elementwise kernels; h and dz quantized with their projections separately",
+            "steps": steps, "warmup": warmup, "data": "synthetic"}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -313,6 +465,17 @@ def main():
     _lib.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.ablation and args.workload == "flux_mlp":
+        print(json.dumps(mlp_ablation(torch, _lib, dev, args.seed, args.steps, args.warmup)), flush=True)
+        return
+    if args.ablation:
+        if args.workload != "flux_qkv":
+            raise SystemExit("--ablation is defined for flux_qkv and flux_mlp")
+        d = gen.layer_inputs_torch(gen.SHAPES["flux_qkv"], args.seed, dev)
+        wq, ws, _ = _lib.ft_quantize_blockwise(d["W"], block_rows=32)
+        print(json.dumps(fusion_ablation(torch, _lib, d, wq, ws, gen.SHAPES["flux_qkv"], args.steps, args.warmup)),
+              flush=True)
+        return
     layers = workload_layers(args.workload)
     b = Builder(torch, _lib, dev, args.seed, random_weights=args.workload == "flux_stack")
     fwd_ops, bwd_ops, counts = [], [], {}
