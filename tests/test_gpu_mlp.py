@@ -211,3 +211,23 @@ def test_mlp_pair_flux_shape_sampled():
     assert np.all(np.abs(host(P2)[rows] - pr) <= proj_bound(F, 48, pa))
     pr, pa = ref.proj(dz[rows], U1, 1)
     assert np.all(np.abs(host(Qp1)[rows] - pr) <= proj_bound(F, 48, pa))
+
+
+def test_mlp_empty_token_axis():
+    """M = 0 through both fused epilogues: the calls succeed and every output
+    with a token axis is empty."""
+    rng = np.random.default_rng(11)
+    K, F, R = 256, 512, 32
+    W1 = dev_bf16(rand_bf16(rng, (F, K), 0.05))
+    W2 = dev_bf16(rand_bf16(rng, (K, F), 0.05))
+    w1q, w1s, _ = _lib.ft_quantize_blockwise(W1, block_rows=32)
+    w2q, w2s, _ = _lib.ft_quantize_blockwise(W2, block_rows=32)
+    xq, xs, _ = _lib.ft_quantize_blockwise(torch.empty((0, K), dtype=torch.bfloat16, device=DEV))
+    D2 = dev_bf16(rand_bf16(rng, (F, R), 0.05))
+    z, h, hq, hs, P2 = _lib.ft_linear_fwd_gelu(xq, xs, w1q, w1s, K, D2=D2)
+    assert z.shape == (0, F) and h.shape == (0, F) and hq.shape == (0, F // 2) and P2.shape == (0, R)
+    gq, gs, _ = _lib.ft_quantize_blockwise(torch.empty((0, K), dtype=torch.bfloat16, device=DEV))
+    U1 = dev_bf16(rand_bf16(rng, (R, F), 0.05))
+    dz, dzq, dzs, Qp1 = _lib.ft_linear_bwd_input_dgelu(gq, gs, w2q, w2s, F, z, U1=U1)
+    torch.cuda.synchronize()
+    assert dz.shape == (0, F) and dzq.shape == (0, F // 2) and Qp1.shape == (0, R)

@@ -216,6 +216,34 @@ def test_lora_grads_accumulate():
     assert torch.equal(dA2, 2 * dA) and torch.equal(dB2, 2 * dB)
 
 
+def test_empty_token_axis():
+    """M = 0: every output with a token axis is empty and the calls succeed; the
+    adapter gradients are sums over no tokens, so they come out as exact zeros,
+    or unchanged when accumulating."""
+    K, N, r = 256, 320, 16
+    rng = np.random.default_rng(5)
+    W = dev_bf16(gen.f32_to_bf16_bits(rng.standard_normal((N, K)).astype(np.float32)))
+    wq, ws, _ = _lib.ft_quantize_blockwise(W, block_rows=32)
+    D = dev_bf16(gen.f32_to_bf16_bits(rng.standard_normal((K, 2 * r)).astype(np.float32)))
+    U = dev_bf16(gen.f32_to_bf16_bits(rng.standard_normal((2 * r, N)).astype(np.float32)))
+    X = torch.empty((0, K), dtype=torch.bfloat16, device=DEV)
+    dY = torch.empty((0, N), dtype=torch.bfloat16, device=DEV)
+    xq, xs, P = _lib.ft_quantize_blockwise(X, proj=D)
+    gq, gs, Qp = _lib.ft_quantize_blockwise(dY, proj=U, proj_layout=_lib.FT_PROJ_R_BY_COLS)
+    assert xq.shape == (0, K // 2) and P.shape == (0, 2 * r) and Qp.shape == (0, 2 * r)
+    y = _lib.ft_linear_fwd(xq, xs, wq, ws, K, P=P, U=U)
+    dx = _lib.ft_linear_bwd_input(gq, gs, wq, ws, K, Qp=Qp, D=D, out_dtype=torch.float32)
+    assert y.shape == (0, N) and dx.shape == (0, K)
+    dA = torch.full((K, r), 7.0, device=DEV)
+    dB = torch.full((r, N), -3.0, device=DEV)
+    _lib.ft_lora_grads(X, dY, P, Qp, r, col0=r, dA=dA, dB=dB, accumulate=True)
+    torch.cuda.synchronize()
+    assert bool((dA == 7.0).all()) and bool((dB == -3.0).all())
+    _lib.ft_lora_grads(X, dY, P, Qp, r, col0=r, dA=dA, dB=dB)
+    torch.cuda.synchronize()
+    assert torch.equal(dA, torch.zeros_like(dA)) and torch.equal(dB, torch.zeros_like(dB))
+
+
 def test_projection_and_lora_grads_are_reproducible():
     """Partial sums over column and token chunks are combined in a fixed order:
     two runs give the same bits."""
