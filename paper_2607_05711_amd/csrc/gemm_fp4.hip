@@ -992,26 +992,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     static_assert(2 * 128 * 64 * 4 <= 4 * STG + PSLICE, "combine area below the code buffers");
     const int R2 = ep.R2;
     const int tn = nt;
-    __syncthreads();  // all waves are done with the ring
-    if (R2 > 0) {
-      // stage the projection slice: rows n0..n0+255 of D2 [NO, R2], or
-      // columns n0..n0+255 of U1 [R2, NO]; zeros outside
-#pragma unroll
-      for (int u = 0; u < 8; u++) {
-        const int sl = tid + 256 * u;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if constexpr (G) {
-          const int rr = sl >> 3, cc = (sl & 7) * 8;
-          if (n0 + rr < NO && cc < R2) v = *(const uint4*)(ep.proj + (size_t)(n0 + rr) * R2 + cc);
-          *(uint4*)(ps + rr * PS1 + cc) = v;
-        } else {
-          const int rr = sl >> 5, cc = (sl & 31) * 8;
-          if (rr < R2 && n0 + cc < NO) v = *(const uint4*)(ep.proj + (size_t)rr * NO + n0 + cc);
-          *(uint4*)(ps + rr * PS2 + cc) = v;
-        }
-      }
-    }
-    __syncthreads();
+    // The projection slice: rows n0..n0+255 of D2 [NO, R2], or columns
+    // n0..n0+255 of U1 [R2, NO]; zeros outside.  EPI_DGELU has registers to
+    // spare: it issues its slice loads, and the first pass's z loads, before
+    // the barrier that frees the ring, so they overlap the wait for the other
+    // waves.  In EPI_GELU, holding the slice across the barrier would spill,
+    // so each of its loads is written to LDS as it arrives, after the barrier.
     const __amdgpu_buffer_rsrc_t r_y = make_rsrc(ep.y, (uint32_t)M * NO * 2);
     const __amdgpu_buffer_rsrc_t r_z = make_rsrc(G ? (const void*)ep.z_out : (const void*)ep.z_in, (uint32_t)M * NO * 2);
     const __amdgpu_buffer_rsrc_t r_q = make_rsrc(ep.q, (uint32_t)M * (NO / 2));
@@ -1031,7 +1017,34 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
             r_z, (gr < M && gc < NO) ? ((uint32_t)gr * NO + gc) * 2 : kOobOffset, 0, 0));
       }
     };
-    if constexpr (!G) load_z(0, zpre[0]);
+    uint4 pv[8];
+    if constexpr (!G) {
+      if (R2 > 0) {
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+          const int sl = tid + 256 * u, rr = sl >> 5, cc = (sl & 31) * 8;
+          pv[u] = make_uint4(0, 0, 0, 0);
+          if (rr < R2 && n0 + cc < NO) pv[u] = *(const uint4*)(ep.proj + (size_t)rr * NO + n0 + cc);
+        }
+      }
+      load_z(0, zpre[0]);
+    }
+    __syncthreads();  // all waves are done with the ring
+    if (R2 > 0) {
+#pragma unroll
+      for (int u = 0; u < 8; u++) {
+        const int sl = tid + 256 * u;
+        if constexpr (G) {
+          const int rr = sl >> 3, cc = (sl & 7) * 8;
+          uint4 v = make_uint4(0, 0, 0, 0);
+          if (n0 + rr < NO && cc < R2) v = *(const uint4*)(ep.proj + (size_t)(n0 + rr) * R2 + cc);
+          *(uint4*)(ps + rr * PS1 + cc) = v;
+        } else {
+          *(uint4*)(ps + (sl >> 5) * PS2 + (sl & 31) * 8) = pv[u];
+        }
+      }
+    }
+    __syncthreads();
 #pragma unroll   // acc[i] must be indexed by constants
     for (int i = 0; i < 4; i++) {
       if constexpr (!G) {
