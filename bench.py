@@ -451,8 +451,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: the layer's data-parallel shards are independent and this "
-              "build runs no collectives; run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only: the layer's data-parallel shards are independent and the "
+              "library runs no collectives; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     if args.copy_calibration:
