@@ -33,6 +33,7 @@ struct LoraGeom {
   static constexpr int SLOT = LG_VBYTES + LBYTES;
   static constexpr int NS = RTJ == 1 ? 3 : 2;             // ring slots
   static constexpr int PD = NS - 1;                       // stages in flight ahead
+  static_assert(PD == 1 || PD == 2, "the prologue issues stages 0 and 1 and the waits allow one stage outstanding");
   static constexpr int V_LOADS = LG_VBYTES / 1024 / 4;    // per wave per stage
   static constexpr int L_LOADS = LBYTES / 1024 / 4;
   static constexpr int LOADS = V_LOADS + L_LOADS;
@@ -219,8 +220,8 @@ __global__ __launch_bounds__(256) void k_lora_grads(LoraJob jb0, LoraJob jb1, in
   else lora_tile<RTJ, false>(job, lds, cg * LG_WC, mbeg, mend, ld, r, part, accumulate);
 }
 
-// Token chunking: enough workgroups for one round (ring LDS allows two per
-// CU up to RTJ 3, one at RTJ 4).
+// Token chunking: enough workgroups for one round.  Every ring takes more
+// than half of LDS (96 KB or more), so a CU holds one workgroup.
 static void lg_geometry(int rows, int K, int N, int r, int& nmch, int& mchunk) {
   const int rtj = (r + 31) / 32;
   const int slot_bytes = LG_VBYTES + LG_BM * rtj * 128, ns = rtj == 1 ? 3 : 2;
