@@ -31,8 +31,10 @@
  *     `stream` (a hipStream_t; NULL = the default stream) and runs
  *     asynchronously.
  *   - bf16 tensors are passed as `const void*` holding IEEE bfloat16 values.
- *   - Every tensor pointer must be 16-byte aligned, except `scales`, `xs`,
- *     `gs`, `ws` (any alignment).
+ *   - Every tensor pointer must be 16-byte aligned, the E8M0 scale arrays
+ *     (`scales`, `xs`, `gs`, `ws`, `hs`, `dzs`) included: the kernels move
+ *     scales in 4- and 16-byte units.  A misaligned pointer gives
+ *     FT_ERR_ALIGN.
  *   - Arguments are validated before anything is enqueued; on error nothing is
  *     launched and the return value says why (ft_last_error() has details).
  *   - FT_ERR_HIP means a launch was rejected by the HIP runtime; earlier
@@ -211,7 +213,7 @@ size_t ft_linear_bwd_input_dgelu_workspace_size(int64_t M, int64_t K, int32_t R1
  *            order (results are reproducible).  Calls sharing a workspace
  *            must not overlap.
  * K, N multiples of 32 and at most 2^24; M >= 0 (M == 0 gives zeros, or
- * leaves dA and dB unchanged when accumulating).
+ * leaves dA and dB unchanged when accumulating).  K == N == 0 is a no-op.
  */
 ft_status ft_lora_grads(const void *x, int64_t M, int64_t K, const void *dy, int64_t N,
                         const float *xa, const float *dyb, int64_t ld, int32_t r,

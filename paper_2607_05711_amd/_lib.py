@@ -42,6 +42,17 @@ def load():
             raise FileNotFoundError(
                 "libfourtune.so is not built (expected at %s); run `python -m paper_2607_05711_amd.build` "
                 "or __graft_entry__.build()" % LIB_PATH)
+        from . import build as _build
+        want = _build.source_hash()
+        try:
+            with open(_build.HASH) as fh:
+                have = fh.read().strip()
+        except OSError:
+            have = None
+        if have != want:
+            raise RuntimeError(
+                "libfourtune.so was not built from the sources in this tree (source hash %s, library built "
+                "from %s); rebuild with `python -m paper_2607_05711_amd.build`" % (want[:16], (have or "?")[:16]))
         L = ctypes.CDLL(LIB_PATH)
         _Z = ctypes.c_size_t
         L.ft_quantize_blockwise.argtypes = [_P, _I64, _I64, _I32, _P, _P, _P, _I32, ctypes.c_int, _P, _P, _Z, _P]

@@ -2,9 +2,14 @@
 
 Every .hip file under csrc/ is compiled to an object in parallel, then linked
 into paper_2607_05711_amd/libfourtune.so.  Packed-fp32 instruction selection
-is disabled for all device code.
+is disabled for all device code, and inline-asm diagnostics are errors.
+
+Next to the library, libfourtune.so.srchash records a SHA-256 over the
+sources, the public header and the compiler flags it was built from; the
+binding refuses to load a library whose record does not match the tree.
 """
 import concurrent.futures
+import hashlib
 import os
 import shutil
 import subprocess
@@ -15,7 +20,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfourtune.so")
+HASH = LIB + ".srchash"
 ARCH = "gfx950"
+HEADER = os.path.join(ROOT, "include", "fourtune.h")
 
 
 def hipcc():
@@ -31,8 +38,22 @@ def sources():
 
 def common_flags():
     return ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
+            "-Werror=inline-asm",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
             "-I", os.path.join(ROOT, "include"), "-I", CSRC]
+
+
+def source_hash():
+    """SHA-256 over every csrc file, the public header and the flags (the
+    paths in the flags are taken relative to the repository)."""
+    h = hashlib.sha256()
+    files = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".h")))
+    for f in files + [HEADER]:
+        h.update(os.path.relpath(f, ROOT).encode() + b"\0")
+        with open(f, "rb") as fh:
+            h.update(fh.read() + b"\0")
+    h.update(" ".join(a.replace(ROOT, ".") for a in common_flags()).encode())
+    return h.hexdigest()
 
 
 def _compile(src):
@@ -54,10 +75,14 @@ def build(verbose=False):
         for _, out in results:
             if out.strip():
                 print(out)
+    digest = source_hash()
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + [o for o, _ in results]
     subprocess.check_call(cmd)
     os.replace(tmp, LIB)
+    with open(HASH + ".tmp", "w") as fh:
+        fh.write(digest + "\n")
+    os.replace(HASH + ".tmp", HASH)
     return LIB
 
 

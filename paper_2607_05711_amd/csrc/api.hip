@@ -92,7 +92,8 @@ ft_status ft_quantize_blockwise(const void* src, int64_t rows, int64_t cols, int
   if (block_rows != 1 && block_rows != 32) return fail(FT_ERR_UNSUPPORTED, "block_rows = %d (1 or 32)", block_rows);
   if (rows == 0 || cols == 0) return FT_OK;
   if (!src || !codes || !scales) return fail(FT_ERR_NULL, "src, codes and scales are required");
-  if (!aligned16(src) || !aligned16(codes)) return fail(FT_ERR_ALIGN, "src or codes not 16-byte aligned");
+  if (!aligned16(src) || !aligned16(codes) || !aligned16(scales))
+    return fail(FT_ERR_ALIGN, "src, codes and scales must be 16-byte aligned");
   if (proj_layout != FT_PROJ_COLS_BY_R && proj_layout != FT_PROJ_R_BY_COLS)
     return fail(FT_ERR_UNSUPPORTED, "proj_layout = %d", (int)proj_layout);
   FT_TRY(check_rank(R, proj, proj_out, "proj", "proj_out"));
@@ -120,8 +121,9 @@ ft_status ft_linear_fwd(const uint8_t* xq, const uint8_t* xs, int64_t M, int64_t
   if (M == 0 || N == 0) return FT_OK;
   if (K == 0) return fail(FT_ERR_SHAPE, "K == 0");
   if (!xq || !xs || !wq || !ws || !y) return fail(FT_ERR_NULL, "xq, xs, wq, ws and y are required");
-  if (!aligned16(xq) || !aligned16(wq) || !aligned16(y) || (bias && !aligned16(bias)))
-    return fail(FT_ERR_ALIGN, "xq, wq, y, bias must be 16-byte aligned");
+  if (!aligned16(xq) || !aligned16(xs) || !aligned16(wq) || !aligned16(ws) || !aligned16(y) ||
+      (bias && !aligned16(bias)))
+    return fail(FT_ERR_ALIGN, "xq, xs, wq, ws, y, bias must be 16-byte aligned");
   FT_TRY(check_rank(R, P, U, "P", "U"));
   return hip_status(ft::launch_gemm_fp4(false, xq, xs, wq, ws, (int)M, (int)N, (int)K, P, R, (const uint16_t*)U,
                                         (const uint16_t*)bias, y, y_dtype == FT_F32, stream),
@@ -139,7 +141,8 @@ ft_status ft_linear_bwd_input(const uint8_t* gq, const uint8_t* gs, int64_t M, i
   if (M == 0 || K == 0) return FT_OK;
   if (N == 0) return fail(FT_ERR_SHAPE, "N == 0");
   if (!gq || !gs || !wq || !ws || !dx) return fail(FT_ERR_NULL, "gq, gs, wq, ws and dx are required");
-  if (!aligned16(gq) || !aligned16(wq) || !aligned16(dx)) return fail(FT_ERR_ALIGN, "gq, wq, dx must be 16-byte aligned");
+  if (!aligned16(gq) || !aligned16(gs) || !aligned16(wq) || !aligned16(ws) || !aligned16(dx))
+    return fail(FT_ERR_ALIGN, "gq, gs, wq, ws, dx must be 16-byte aligned");
   FT_TRY(check_rank(R, Qp, D, "Qp", "D"));
   return hip_status(ft::launch_gemm_fp4(true, gq, gs, wq, ws, (int)M, (int)N, (int)K, Qp, R, (const uint16_t*)D,
                                         nullptr, dx, dx_dtype == FT_F32, stream),
@@ -165,8 +168,9 @@ ft_status ft_linear_fwd_gelu(const uint8_t* xq, const uint8_t* xs, int64_t M, in
   if (M == 0 || N == 0) return FT_OK;
   if (K == 0) return fail(FT_ERR_SHAPE, "K == 0");
   if (!xq || !xs || !wq || !ws || !z || !h || !hq || !hs) return fail(FT_ERR_NULL, "xq, xs, wq, ws, z, h, hq, hs are required");
-  if (!aligned16(xq) || !aligned16(wq) || !aligned16(z) || !aligned16(h) || !aligned16(hq) || (bias && !aligned16(bias)))
-    return fail(FT_ERR_ALIGN, "xq, wq, z, h, hq, bias must be 16-byte aligned");
+  if (!aligned16(xq) || !aligned16(xs) || !aligned16(wq) || !aligned16(ws) || !aligned16(z) || !aligned16(h) ||
+      !aligned16(hq) || !aligned16(hs) || (bias && !aligned16(bias)))
+    return fail(FT_ERR_ALIGN, "xq, xs, wq, ws, z, h, hq, hs, bias must be 16-byte aligned");
   FT_TRY(check_rank(R, P, U, "P", "U"));
   if (R2 != 0 && (R2 < 16 || R2 > 64 || R2 % 16 != 0)) return fail(FT_ERR_UNSUPPORTED, "R2 = %d: need 0 or 16..64, R2 %% 16 == 0", R2);
   FT_TRY(check_rank(R2, D2, P2, "D2", "P2"));
@@ -194,8 +198,9 @@ ft_status ft_linear_bwd_input_dgelu(const uint8_t* gq, const uint8_t* gs, int64_
   if (N == 0) return fail(FT_ERR_SHAPE, "N == 0");
   if (!gq || !gs || !wq || !ws || !z || !dz || !dzq || !dzs)
     return fail(FT_ERR_NULL, "gq, gs, wq, ws, z, dz, dzq, dzs are required");
-  if (!aligned16(gq) || !aligned16(wq) || !aligned16(z) || !aligned16(dz) || !aligned16(dzq))
-    return fail(FT_ERR_ALIGN, "gq, wq, z, dz, dzq must be 16-byte aligned");
+  if (!aligned16(gq) || !aligned16(gs) || !aligned16(wq) || !aligned16(ws) || !aligned16(z) || !aligned16(dz) ||
+      !aligned16(dzq) || !aligned16(dzs))
+    return fail(FT_ERR_ALIGN, "gq, gs, wq, ws, z, dz, dzq, dzs must be 16-byte aligned");
   FT_TRY(check_rank(R, Qp, D, "Qp", "D"));
   if (R1 != 0 && (R1 < 16 || R1 > 64 || R1 % 16 != 0)) return fail(FT_ERR_UNSUPPORTED, "R1 = %d: need 0 or 16..64, R1 %% 16 == 0", R1);
   FT_TRY(check_rank(R1, U1, Qp1, "U1", "Qp1"));
@@ -227,6 +232,7 @@ ft_status ft_lora_grads(const void* x, int64_t M, int64_t K, const void* dy, int
   if (r < 1 || r > 128) return fail(FT_ERR_UNSUPPORTED, "r = %d: need 1 <= r <= 128", r);
   if (ld < r || ld % 4 != 0 || ld > 4096) return fail(FT_ERR_SHAPE, "ld = %lld: need r <= ld <= 4096, ld %% 4 == 0", (long long)ld);
   if (accumulate != 0 && accumulate != 1) return fail(FT_ERR_UNSUPPORTED, "accumulate = %d", accumulate);
+  if (K == 0 && N == 0) return FT_OK;   // dA [0, r] and dB [r, 0] hold nothing
   if (!dA || !dB) return fail(FT_ERR_NULL, "dA and dB are required");
   if (M > 0 && (!x || !dy || !xa || !dyb)) return fail(FT_ERR_NULL, "x, dy, xa and dyb are required");
   if (K > (1 << 24) || N > (1 << 24)) return fail(FT_ERR_UNSUPPORTED, "K and N above 2^24 are not supported here");

@@ -116,38 +116,6 @@ __device__ __forceinline__ uint32_t quad_quantize8(const uint32_t (&w)[4], uint3
 }
 
 
-// Quantize 32 bf16 values (16 dwords, element 2i in the low half of dword i)
-// to 16 bytes of packed E2M1 codes; returns the E8M0 code.  The conversion
-// instruction divides by the scale, rounds to nearest even and saturates,
-// copying the sign, which is the block rule of the library.
-__device__ __forceinline__ uint32_t quantize32(const uint32_t (&w)[16], uint32_t (&out)[4]) {
-  uint32_t m = 0;
-#pragma unroll
-  for (int i = 0; i < 16; i++) {
-    uint32_t a = w[i] & 0x7FFF7FFFu;
-    uint32_t lo = a & 0xFFFFu, hi = a >> 16;
-    m = max(m, max(lo, hi));
-  }
-  const uint32_t code = e8m0_from_amax_bits(m);
-  const float s = e8m0_to_f32(code);
-#pragma unroll
-  for (int d = 0; d < 4; d++) {
-    uint32_t o = 0;
-    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[4 * d + 0]), s, 0);
-    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[4 * d + 1]), s, 1);
-    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[4 * d + 2]), s, 2);
-    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[4 * d + 3]), s, 3);
-    out[d] = o;
-  }
-  return code;
-}
-
-// 16-byte streaming load (non-temporal hint: the data is read once).
-__device__ __forceinline__ uint4 load_nt16(const void* p) {
-  const v4i v = __builtin_nontemporal_load((const v4i*)p);
-  return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
-}
-
 __device__ __forceinline__ v4s lds_read_tr16(const FT_LDS void* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((FT_LDS v4s*)p);
 }
@@ -192,21 +160,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 // An offset no buffer here reaches: a load from it returns zeros.
 constexpr uint32_t kOobOffset = 0x80000000u;
 
-// 16 bytes per lane from a buffer into LDS at lds_base + 16 * lane
-// (lds_base must be the same for the whole wave).
-__device__ __forceinline__ void buffer_to_lds16(__amdgpu_buffer_rsrc_t r, FT_LDS void* lds_base, uint32_t voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_base, 16, voff, 0, 0, 0);
-}
-
-__device__ __forceinline__ uint2 buffer_load8(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
-  const v2i v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, 0, 0);
-  return make_uint2((uint32_t)v[0], (uint32_t)v[1]);
-}
-
-__device__ __forceinline__ uint32_t buffer_load_u8(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
-  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(r, voff, 0, 0);
-}
-
 // Buffer resource words for the asm loads below (same layout as make_rsrc).
 __device__ __forceinline__ v4i rsrc_words(const void* base, uint32_t bytes) {
   const uint64_t a = (uint64_t)base;
@@ -233,17 +186,28 @@ __device__ __forceinline__ void wait_vm() {
 // buffer size reads zeros whatever soff is.
 // The uniform operands pass through readfirstlane: the compiler may hold a
 // uniform value in a VGPR, which an "s" asm operand would not convert.
-// An LDS DMA needs one wait state after a scalar write of M0 (the compiler
-// inserts it for the loads it generates, not inside an asm block).
+// The LDS destination travels in M0, which the compiler reserves: the asm
+// saves M0 in a scratch SGPR and restores it after the load has issued (the
+// load reads M0 at issue), so M0 holds the same value before and after the
+// statement whatever the compiler keeps there.  An LDS DMA needs one wait
+// state after a scalar write of M0.
 __device__ __forceinline__ void dma16(v4i rsrc, uint32_t lds_base, uint32_t voff, uint32_t soff) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc),
-                  "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
+  uint32_t keep;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+               "buffer_load_dwordx4 %2, %3, %4 offen lds\n\ts_mov_b32 m0, %0"
+               : "=&s"(keep)
+               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc),
+                 "s"(__builtin_amdgcn_readfirstlane(soff))
+               : "memory");
 }
 __device__ __forceinline__ void dma4(v4i rsrc, uint32_t lds_base, uint32_t voff, uint32_t soff) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, %3 offen lds"
-               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc),
-                  "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
+  uint32_t keep;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+               "buffer_load_dword %2, %3, %4 offen lds\n\ts_mov_b32 m0, %0"
+               : "=&s"(keep)
+               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc),
+                 "s"(__builtin_amdgcn_readfirstlane(soff))
+               : "memory");
 }
 
 }  // namespace ft

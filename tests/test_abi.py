@@ -71,6 +71,8 @@ def test_quantize_validation():
     assert q(ALIGNED, 4, 64, 2, ALIGNED, ALIGNED) == _lib.FT_ERR_UNSUPPORTED
     assert q(NULL, 4, 64, 1, ALIGNED, ALIGNED) == _lib.FT_ERR_NULL
     assert q(MISALIGNED, 4, 64, 1, ALIGNED, ALIGNED) == _lib.FT_ERR_ALIGN
+    assert q(ALIGNED, 4, 64, 1, ALIGNED, MISALIGNED) == _lib.FT_ERR_ALIGN      # scales too
+    assert q(ALIGNED, 64, 64, 32, ALIGNED, ctypes.c_void_p(0x100004)) == _lib.FT_ERR_ALIGN
     assert q(ALIGNED, 4, 64, 1, ALIGNED, ALIGNED, ALIGNED2, 20, 0, ALIGNED2) == _lib.FT_ERR_UNSUPPORTED
     assert q(ALIGNED, 4, 64, 1, ALIGNED, ALIGNED, ALIGNED2, 144, 0, ALIGNED2) == _lib.FT_ERR_UNSUPPORTED
     assert q(ALIGNED, 4, 64, 1, ALIGNED, ALIGNED, ALIGNED2, 32, 0, NULL) == _lib.FT_ERR_NULL
@@ -106,6 +108,9 @@ def test_linear_validation():
     assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 3, NULL) == _lib.FT_ERR_UNSUPPORTED
     assert f(ALIGNED, NULL, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_NULL
     assert f(MISALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_ALIGN
+    # the scale arrays are moved in 4- and 16-byte units: they must be aligned like the rest
+    assert f(ALIGNED, MISALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_ALIGN
+    assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, MISALIGNED, 64, NULL, 0, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_ALIGN
     assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, ALIGNED2, 32, NULL, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_NULL
     assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, ALIGNED2, 24, ALIGNED2, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_UNSUPPORTED
     assert f(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, ALIGNED2, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_UNSUPPORTED
@@ -115,6 +120,8 @@ def test_linear_validation():
     assert b(ALIGNED, ALIGNED, 8, 48, ALIGNED, ALIGNED, 64, NULL, 0, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_SHAPE
     assert b(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, ALIGNED2, 32, NULL, ALIGNED, 0, NULL) == _lib.FT_ERR_NULL
     assert b(ALIGNED, ALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, MISALIGNED, 1, NULL) == _lib.FT_ERR_ALIGN
+    assert b(ALIGNED, MISALIGNED, 8, 64, ALIGNED, ALIGNED, 64, NULL, 0, NULL, ALIGNED, 1, NULL) == _lib.FT_ERR_ALIGN
+    assert b(ALIGNED, ALIGNED, 8, 64, ALIGNED, MISALIGNED, 64, NULL, 0, NULL, ALIGNED, 1, NULL) == _lib.FT_ERR_ALIGN
     assert b(NULL, NULL, 0, 64, NULL, NULL, 64, NULL, 0, NULL, NULL, 0, NULL) == _lib.FT_OK
 
 
@@ -136,6 +143,10 @@ def test_lora_validation():
     assert f(*args(xa=MISALIGNED)) == _lib.FT_ERR_ALIGN
     assert f(*args(dyb=MISALIGNED)) == _lib.FT_ERR_ALIGN
     assert f(*args(N=(1 << 24) + 32)) == _lib.FT_ERR_UNSUPPORTED
+    # no output columns at all: nothing to compute (the token-window sizing divides by max(K, N))
+    assert f(*args(K=0, N=0)) == _lib.FT_OK
+    assert f(*args(K=0, N=0, dA=NULL, dB=NULL, x=NULL, dy=NULL)) == _lib.FT_OK
+    assert _lib.ft_lora_grads_workspace_size(4608, 0, 0, 64, 32) == 0
     # token chunks leave partial sums in the workspace
     need = _lib.ft_lora_grads_workspace_size(4608, 3072, 9216, 64, 32)
     assert need > 0 and need % (32 * (3072 + 9216) * 4) == 0
@@ -161,6 +172,8 @@ def test_mlp_fused_validation():
     assert call(R2=32, D2=ALIGNED2) == _lib.FT_ERR_NULL
     assert call(h=NULL) == _lib.FT_ERR_NULL
     assert call(z=MISALIGNED) == _lib.FT_ERR_ALIGN
+    assert call(xs=MISALIGNED) == _lib.FT_ERR_ALIGN
+    assert call(hs=MISALIGNED) == _lib.FT_ERR_ALIGN
     need = _lib.ft_linear_fwd_gelu_workspace_size(4608, 12288, 64)
     assert need == 48 * 4608 * 64 * 4                                  # one partial per 256-column tile
     assert _lib.ft_linear_fwd_gelu_workspace_size(4608, 256, 64) == 0  # one tile: written directly
@@ -175,6 +188,18 @@ def test_mlp_fused_validation():
     assert call_b(N=160) == _lib.FT_ERR_UNSUPPORTED                   # reduction not a multiple of 128
     assert call_b(K=224) == _lib.FT_ERR_UNSUPPORTED
     assert call_b(z=NULL) == _lib.FT_ERR_NULL
+    assert call_b(gs=MISALIGNED) == _lib.FT_ERR_ALIGN
+    assert call_b(dzs=MISALIGNED) == _lib.FT_ERR_ALIGN
     assert call_b(R1=48, U1=ALIGNED2) == _lib.FT_ERR_NULL
     assert _lib.ft_linear_bwd_input_dgelu_workspace_size(4608, 12288, 64) == 48 * 4608 * 64 * 4
     assert call_b(M=0) == _lib.FT_OK
+
+
+def test_load_refuses_a_library_built_from_other_sources(monkeypatch):
+    """The binding ties the shared library to the sources in the tree: a
+    library whose recorded source hash differs is refused, never loaded."""
+    from paper_2607_05711_amd import build
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(build, "source_hash", lambda: "0" * 64)
+    with pytest.raises(RuntimeError, match="not built from the sources"):
+        _lib.load()

@@ -77,16 +77,23 @@ def test_bwd_exact_rational():
     wq, ws = random_codes(rng, N, K, 32)
     Qp = rng.integers(-64, 64, (M, R)) / 8.0
     D = f32_to_bf16_bits((rng.integers(-64, 64, (K, R)) / 16.0).astype(np.float32))
-    dx, _ = ref.linear_bwd_input(gq, gs, wq, ws, K, Qp, D)
+    dx, s = ref.linear_bwd_input(gq, gs, wq, ws, K, Qp, D)
     gc, wc = unpack(gq), unpack(wq)
     for m in range(M):
         for k in range(K):
             acc = Fraction(0)
+            mag = Fraction(0)
             for n in range(N):
-                acc += frac_code(int(gc[m, n]), int(gs[m, n // 32])) * frac_code(int(wc[n, k]), int(ws[n // 32, k // 32]))
+                t = frac_code(int(gc[m, n]), int(gs[m, n // 32])) * frac_code(int(wc[n, k]), int(ws[n // 32, k // 32]))
+                acc += t
+                mag += abs(t)
             for j in range(R):
-                acc += Fraction(Qp[m, j]) * frac_bf16(D[k, j])
+                t = Fraction(Qp[m, j]) * frac_bf16(D[k, j])
+                acc += t
+                mag += abs(t)
             assert Fraction(dx[m, k]) == acc, (m, k)
+            # the magnitude sum sets every dX tolerance: pinned exactly as well
+            assert Fraction(s[m, k]) == mag, (m, k)
 
 
 def test_proj_and_lora_exact_rational():
@@ -104,13 +111,15 @@ def test_proj_and_lora_exact_rational():
             assert Fraction(p[i, j]) == want
             assert Fraction(pabs[i, j]) == sum(abs(frac_bf16(x[i, k]) * frac_bf16(d[k, j])) for k in range(K))
             assert Fraction(qp[i, j]) == sum(frac_bf16(g[i, n]) * frac_bf16(u[j, n]) for n in range(N))
-    dA, dB, _, _ = ref.lora_grads(x, g, p, qp)
+    dA, dB, sA, sB = ref.lora_grads(x, g, p, qp)
     for k in range(K):
         for j in range(r):
             assert Fraction(dA[k, j]) == sum(frac_bf16(x[m, k]) * Fraction(qp[m, j]) for m in range(M))
+            assert Fraction(sA[k, j]) == sum(abs(frac_bf16(x[m, k]) * Fraction(qp[m, j])) for m in range(M))
     for j in range(r):
         for n in range(N):
             assert Fraction(dB[j, n]) == sum(Fraction(p[m, j]) * frac_bf16(g[m, n]) for m in range(M))
+            assert Fraction(sB[j, n]) == sum(abs(Fraction(p[m, j]) * frac_bf16(g[m, n])) for m in range(M))
 
 
 def test_fwd_bwd_against_numpy():
@@ -136,6 +145,18 @@ def test_fwd_bwd_against_numpy():
     dx, sdx = ref.linear_bwd_input(gq, gs, wq, ws, K, Qp, D, Qpabs=Qpabs)
     dx_np = Gd @ Wd + f64(g) @ f64(U).T @ f64(D).T
     assert np.all(np.abs(dx - dx_np) <= 1e-12 * sdx)
+    # S of Eq. (3) expands the low-rank term over (n, j): |G| |U|^T |D|^T, not |Qp| |D|^T
+    sdx_np = np.abs(Gd) @ np.abs(Wd) + (np.abs(f64(g)) @ np.abs(f64(U)).T) @ np.abs(f64(D)).T
+    assert np.allclose(sdx, sdx_np, rtol=1e-12, atol=0)
+    assert not np.allclose(sdx, np.abs(Gd) @ np.abs(Wd) + np.abs(Qp) @ np.abs(f64(D)).T, rtol=1e-6)
+    # adapter-gradient magnitudes: |X|^T |G B^T| and |X A|^T |G|
+    r, rs = 16, 16
+    dA, dB, sA, sB = ref.lora_grads(x, g, P[:, rs:], Qp[:, rs:])
+    assert np.allclose(sA, np.abs(f64(x)).T @ np.abs(Qp[:, rs:]), rtol=1e-12, atol=0)
+    assert np.allclose(sB, np.abs(P[:, rs:]).T @ np.abs(f64(g)), rtol=1e-12, atol=0)
+    assert np.all(np.abs(dA - f64(x).T @ Qp[:, rs:]) <= 1e-12 * sA)
+    assert np.all(np.abs(dB - P[:, rs:].T @ f64(g)) <= 1e-12 * sB)
+    assert r + rs == R
 
 
 def test_ste_special_case_matches_autograd():
