@@ -14,6 +14,13 @@ ft_linear_bwd_input, so:
     GPU's h / dz;
   * P2 / Qp1 are within the fp32 accumulation bound of the oracle projection of
     the GPU's h / dz (partial sums per 256-column tile).
+Those checks follow the chain stage by stage.  The chain is also anchored on
+oracle-only intermediates: z_or = RNE_bf16(y_oracle), taken wherever no bf16
+rounding midpoint lies within the forward's tolerance 1e-5 * S of y_oracle (the
+fused z must equal it there, and be one of the two neighbours elsewhere);
+h_or = GELU(z_or) and dz_or = dH_oracle * GELU'(z) in fp64; the fused outputs
+must lie within one bf16 unit of them, and the projections within the fp32
+bound plus what the one-unit differences can move them.
 """
 import numpy as np
 import pytest
@@ -52,6 +59,22 @@ def rne_bf16_f64(a):
 def within_one_unit(gpu_bits, ref_f64, abs_slack):
     g, r = f64(gpu_bits), np.asarray(ref_f64, dtype=np.float64)
     return np.abs(g - r) <= 2.0 ** -7 * np.abs(r) + abs_slack
+
+
+def anchored_z(z, yr, S):
+    """Check the fused z against the oracle's forward: z == RNE_bf16(yr) where
+    the rounding is decided within the tolerance, else one of the two bf16
+    values the tolerance interval rounds to.  Returns (z_or, sure)."""
+    tol = 1e-5 * S
+    lo, hi = rne_bf16_f64(yr - tol), rne_bf16_f64(yr + tol)
+    sure = lo == hi
+    z_or = rne_bf16_f64(yr)
+    assert np.array_equal(z[sure], z_or[sure]), "z differs from RNE_bf16 of the oracle's forward"
+    assert np.all((z == lo) | (z == hi)), "z outside the rounding interval of the oracle's forward"
+    # 1e-5 * S spans a sizeable part of a bf16 unit where S >> |y|: most but
+    # not all roundings are decided
+    assert sure.mean() > 0.5, sure.mean()
+    return z_or, sure
 
 
 def rand_bf16(rng, shape, scale):
@@ -112,11 +135,24 @@ def test_fc1_forward_gelu_quantize_project(M, K, N, R, R2):
     q, s = ref.quantize(h, 1)
     assert np.array_equal(hq, q) and np.array_equal(hs, s)
 
+    # anchored on the oracle alone: z_or from the oracle's forward, h_or = GELU(z_or)
+    z_or, sure = anchored_z(z, yr, S)
+    h_or = ref.gelu(f64(z_or))
+    ok = within_one_unit(h[sure], h_or[sure], 1e-6 * np.abs(f64(z_or[sure])))
+    assert ok.all(), "h: %d of %d outside one bf16 unit of GELU(z_oracle)" % ((~ok).sum(), ok.size)
+
     # FC2's down-projection of h
     if R2:
         pr, pa = ref.proj(h, D2, 0)
         tiles = (N + 255) // 256
-        assert np.all(np.abs(host(P2).astype(np.float64) - pr) <= proj_bound(N, tiles, pa))
+        P2h = host(P2).astype(np.float64)
+        assert np.all(np.abs(P2h - pr) <= proj_bound(N, tiles, pa))
+        # against h_or = bf16(GELU(z_or)) built by the oracle: the fp32 bound plus
+        # what the elements where h and h_or differ (at most one unit) contribute
+        h_or16 = rne_bf16_f64(h_or)
+        pr_or, pa_or = ref.proj(h_or16, D2, 0)
+        moved = np.abs(f64(h) - f64(h_or16)) @ np.abs(f64(D2))
+        assert np.all(np.abs(P2h - pr_or) <= proj_bound(N, tiles, pa_or) + moved * (1 + 1e-6))
 
 
 BWD_CASES = [  # M, N (FC2 output width), K (MLP width), R, R1
@@ -167,6 +203,14 @@ def test_fc2_backward_dgelu_quantize_project(M, N, K, R, R1):
     q, s = ref.quantize(dz, 1)
     assert np.array_equal(dzq, q) and np.array_equal(dzs, s)
 
+    # anchored on the oracle alone: dz_or = dH_oracle * GELU'(z) in fp64; the
+    # GPU's dH carries at most 1e-5 * S, and its bf16 rounding one unit
+    gp = ref.gelu(f64(Z), derivative=True)
+    dz_or = dhr * gp
+    lim = 2.0 ** -7 * np.abs(dz_or) + 1.01e-5 * S * np.abs(gp) + 1e-6 * np.abs(dhr) + 1e-30
+    ok = np.abs(f64(dz) - dz_or) <= lim
+    assert ok.all(), "dz: %d of %d outside one bf16 unit of dH_oracle GELU'(z)" % ((~ok).sum(), ok.size)
+
     if R1:
         pr, pa = ref.proj(dz, U1, 1)
         tiles = (K + 255) // 256
@@ -175,8 +219,10 @@ def test_fc2_backward_dgelu_quantize_project(M, N, K, R, R1):
 
 def test_mlp_pair_flux_shape_sampled():
     """FLUX.1-dev MLP at 1024^2 (M = 4608, 3072 -> 12288 -> 3072, ranks 32 + 32)
-    in the launch configuration the benchmark times: quantized outputs and
-    projections in full, elementwise outputs on sampled rows."""
+    in the launch configuration the benchmark times: quantized outputs in full;
+    FC1's output and FC2's input gradient against the oracle, and the
+    elementwise outputs and projections anchored on the oracle, on the last
+    256-row tile and scattered rows."""
     M, D_, F = 4608, 3072, 12288
     rng = np.random.default_rng(11)
     X = rand_bf16(rng, (M, D_), 1.0)
@@ -201,7 +247,7 @@ def test_mlp_pair_flux_shape_sampled():
     assert np.array_equal(hq, q) and np.array_equal(hs, s)
     q, s = ref.quantize(dz, 1)
     assert np.array_equal(dzq, q) and np.array_equal(dzs, s)
-    rows = np.array([0, 1, 777, 2048, 4095, 4607])
+    rows = np.unique(np.concatenate([[0, 1, 777, 2048, 4095], np.arange(4352, 4608)]))
     href = ref.gelu(f64(z[rows]))
     assert within_one_unit(h[rows], href, 1e-6 * np.abs(f64(z[rows]))).all()
     dh = host(dh32)[rows].astype(np.float64)
@@ -211,6 +257,32 @@ def test_mlp_pair_flux_shape_sampled():
     assert np.all(np.abs(host(P2)[rows] - pr) <= proj_bound(F, 48, pa))
     pr, pa = ref.proj(dz[rows], U1, 1)
     assert np.all(np.abs(host(Qp1)[rows] - pr) <= proj_bound(F, 48, pa))
+
+    # anchored on the oracle: FC1's output from the oracle's quantization and
+    # forward of these rows, then z_or, h_or = GELU(z_or); FC2's input gradient
+    # from the oracle's backward, dz_or = dH_oracle GELU'(z_or)
+    xq_o, xs_o = ref.quantize(X[rows], 1)
+    w1q_o, w1s_o = ref.quantize(W1, 32)
+    P1r, P1a = ref.proj(X[rows], D1, 0)
+    yr, S = ref.linear_fwd(xq_o, xs_o, w1q_o, w1s_o, D_, P1r, U1, b1, Pabs=P1a)
+    y32r = host(y32)[rows].astype(np.float64)
+    assert np.all(np.abs(y32r - yr) <= 1e-5 * S), "FC1 output outside 1e-5 * S"
+    z_or, sure = anchored_z(z[rows], yr, S)
+    h_or = ref.gelu(f64(z_or))
+    assert within_one_unit(h[rows][sure], h_or[sure], 1e-6 * np.abs(f64(z_or[sure]))).all()
+    gq_o, gs_o = ref.quantize(dY[rows], 1)
+    w2q_o, w2s_o = ref.quantize(W2, 32)
+    Q2r, Q2a = ref.proj(dY[rows], U2, 1)
+    dhr, Sdh = ref.linear_bwd_input(gq_o, gs_o, w2q_o, w2s_o, F, Q2r, D2, Qpabs=Q2a)
+    assert np.all(np.abs(dh - dhr) <= 1e-5 * Sdh), "FC2 input gradient outside 1e-5 * S"
+    gp = ref.gelu(f64(z_or), derivative=True)
+    dz_or = dhr * gp
+    lim = 2.0 ** -7 * np.abs(dz_or) + 1.01e-5 * Sdh * np.abs(gp) + 1e-6 * np.abs(dhr) + 1e-30
+    assert np.all((np.abs(f64(dz[rows]) - dz_or) <= lim)[sure]), "dz outside one bf16 unit of the oracle's"
+    h_or16 = rne_bf16_f64(h_or)
+    pr_or, pa_or = ref.proj(h_or16, D2, 0)
+    moved = np.abs(f64(h[rows]) - f64(h_or16)) @ np.abs(f64(D2))
+    assert np.all(np.abs(host(P2)[rows] - pr_or) <= proj_bound(F, 48, pa_or) + moved * (1 + 1e-6))
 
 
 def test_mlp_empty_token_axis():

@@ -195,7 +195,11 @@ def test_layer_tiny_svd_stabilizer():
 
 
 @pytest.mark.parametrize("M,K,N,r,rs", [(300, 640, 608, 16, 32), (1, 32, 32, 16, 16), (257, 288, 544, 32, 0),
-                                        (64, 512, 256, 0, 0), (520, 1056, 800, 64, 32), (33, 96, 1312, 8, 8)])
+                                        (64, 512, 256, 0, 0), (520, 1056, 800, 64, 32), (33, 96, 1312, 8, 8),
+                                        # both reductions multiples of 512 (the A scales of two stages load
+                                        # together, the kernels the benchmark times), 3x6 forward and 3x4
+                                        # backward tiles with a ragged last row tile, R = 64 and a bias
+                                        (520, 1024, 1536, 32, 32)])
 def test_layer_ragged(M, K, N, r, rs):
     shape = gen.custom_shape(M, K, N, r=r, r_s=rs, n_outliers=3, outlier_scale=30.0, dy_kind="student_t3")
     d = make_case(shape, 1)
@@ -314,7 +318,9 @@ def test_gemm_random_codes():
 
 
 @pytest.mark.parametrize("M,K,N,R", [(300, 640, 384, 48), (129, 128, 128, 16), (257, 1280, 896, 80),
-                                     (64, 2304, 640, 0), (520, 1408, 1152, 128), (256, 768, 512, 32)])
+                                     (64, 2304, 640, 0), (520, 1408, 1152, 128), (256, 768, 512, 32),
+                                     # paired A-scale stages in both directions, 2x2 tiles and more, R = 64
+                                     (520, 1024, 1536, 64), (512, 2048, 512, 64)])
 def test_gemm_pipelined_shapes(M, K, N, R):
     """Reduction lengths that are multiples of 128 run the pipelined kernel:
     stage counts from one to nine, a half last stage (length an odd multiple
@@ -355,12 +361,16 @@ def test_gemm_pipelined_shapes(M, K, N, R):
 def test_layer_flux_qkv_full_size_sampled():
     """FLUX.1-dev QKV projection at 1024^2 (M=4608, K=3072, N=9216, r = r_s = 32)
     in the launch configuration the benchmark times: quantized operands
-    compared in full, GEMM outputs on sampled rows (including the last),
-    adapter gradients in full."""
+    compared in full, GEMM outputs on two whole 256-row tiles (an interior one
+    and the last) and scattered rows, adapter gradients in full."""
     shape = gen.SHAPES["flux_qkv"]
     d = make_case(shape, 0)
     g = run_gpu_layer(d, shape)
-    rows = np.array([0, 1, 31, 32, 255, 256, 1000, 2047, 3333, 4095, 4096, 4600, 4607])
+    # every row of an interior 256-row tile and of the last one (each output
+    # position of the 256x256 tile, i.e. every wave and accumulator slot), plus
+    # scattered rows
+    rows = np.unique(np.concatenate([[0, 1, 31, 32, 255, 256, 1000, 3333, 4095],
+                                     np.arange(2048, 2304), np.arange(4352, 4608)]))
     wq, ws = ref.quantize(d["W"], 32)
     assert np.array_equal(g["wq"], wq) and np.array_equal(g["ws"], ws)
     xq, xs = ref.quantize(d["X"], 1)
@@ -381,11 +391,13 @@ def test_layer_flux_single_stream_full_size_sampled(name):
     """FLUX.1-dev single-stream block linears at batch 4 (M = 18432 tokens;
     3072 -> 21504 and 15360 -> 3072; LoRA rank 64, stabilizer rank 32), as in
     the stack step: quantized operands and adapter gradients in full, GEMM
-    outputs on sampled rows."""
+    outputs on two whole 256-row tiles (an interior one and the last) and
+    scattered rows."""
     shape = gen.SHAPES[name]
     d = make_case(shape, 4)
     g = run_gpu_layer(d, shape)
-    rows = np.array([0, 255, 256, 5000, 9999, 18175, 18431])
+    rows = np.unique(np.concatenate([[0, 255, 256, 5000, 9999],
+                                     np.arange(9984, 10240), np.arange(18176, 18432)]))
     xq, xs = ref.quantize(d["X"], 1)
     assert np.array_equal(g["xq"], xq) and np.array_equal(g["xs"], xs)
     gq, gs = ref.quantize(d["dY"], 1)
