@@ -45,10 +45,12 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="flux_qkv", choices=["flux_qkv", "flux_mlp", "flux_single", "flux_stack"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="flux_qkv: skip the flux_mlp / flux_single / flux_stack measurements under other_workloads")
     ap.add_argument("--cpu-rows", type=int, default=0, help="token rows in the oracle sample (0: auto)")
     ap.add_argument("--ablation", action="store_true",
                     help="flux_qkv / flux_mlp: time the fused step against an unfused one, print one JSON line, exit")
@@ -476,16 +478,62 @@ def main():
         print(json.dumps(fusion_ablation(torch, _lib, d, wq, ws, gen.SHAPES["flux_qkv"], args.steps, args.warmup)),
               flush=True)
         return
-    layers = workload_layers(args.workload)
-    b = Builder(torch, _lib, dev, args.seed, random_weights=args.workload == "flux_stack")
+    rec = measure_workload(torch, _lib, gen, dev, args.workload, args.steps, args.warmup, args.seed)
+    d = rec.pop("_inputs")
+    out = {
+        "metric": "fused W4A4 linear fwd+bwd TFLOP/s at FLUX 1024^2 shapes; % MXFP4 MFMA peak",
+        "value": rec["tflops"],
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": rec["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "mxfp4",
+        "data": "synthetic",
+        "config": rec["config"],
+    }
+    out.update({k: v for k, v in rec.items() if k not in ("tflops", "ms_per_step", "config")})
+    if args.workload == "flux_qkv" and not args.no_other_workloads:
+        # the other FLUX configurations, each as its own whole step (fewer steps)
+        others = {}
+        for name, st, wu in (("flux_mlp", 20, 10), ("flux_single", 10, 5), ("flux_stack", 3, 2)):
+            o = measure_workload(torch, _lib, gen, dev, name, st, wu, args.seed, per_kernel=name != "flux_stack")
+            o.pop("_inputs")
+            others[name] = {"ms_per_step": o["ms_per_step"], "tflops": o["tflops"],
+                            "pct_mxfp4_peak": o["pct_mxfp4_peak"], "steps": st, "warmup": wu,
+                            "step_ms": o["step_ms"], "workload": o["config"]["workload"]}
+            for k in ("kernels_us", "kernels_frac", "kernels_frac_flushed"):
+                if k in o:
+                    others[name][k] = o[k]
+            torch.cuda.empty_cache()
+            print("measured %s: %.3f ms/step" % (name, o["ms_per_step"]), file=sys.stderr, flush=True)
+        out["other_workloads"] = others
+    if not args.no_cpu_baseline:
+        if d is None:
+            shape = gen.SHAPES["flux_qkv"]
+            d = gen.layer_inputs_torch(shape, args.seed, dev)
+        out["cpu_baseline"] = cpu_baseline(d, gen.SHAPES["flux_qkv"], args.cpu_rows)
+        if args.workload != "flux_qkv":
+            out["cpu_baseline"]["sample"] += " (the QKV linear, the oracle's per-linear rate)"
+    print(json.dumps(out), flush=True)
+
+
+def measure_workload(torch, _lib, gen, dev, workload, steps, warmup, seed, per_kernel=True):
+    """Build one workload's buffers, time its step, and return the measured
+    figures (the layers' inputs for flux_qkv under "_inputs")."""
+    layers = workload_layers(workload)
+    b = Builder(torch, _lib, dev, seed, random_weights=workload == "flux_stack")
     fwd_ops, bwd_ops, counts = [], [], {}
     d = given = None
-    if args.workload == "flux_qkv":
+    if workload == "flux_qkv":
         # the headline layer keeps the seeded recipe of the parity tests
-        d = gen.layer_inputs_torch(gen.SHAPES["flux_qkv"], args.seed, dev)
+        d = gen.layer_inputs_torch(gen.SHAPES["flux_qkv"], seed, dev)
         wq, ws, _ = _lib.ft_quantize_blockwise(d["W"], block_rows=32)     # offline weight preparation
         given = dict(X=d["X"], dY=d["dY"], wq=wq, ws=ws, D=d["D"], U=d["U"], bias=d["bias"])
-    lanes = workload_lanes(args.workload, layers)
+    lanes = workload_lanes(workload, layers)
     for (kind, M, K, N, r, rs), (_, lane) in zip(layers, lanes):
         b.lane = lane
         if kind == "linear":
@@ -538,15 +586,22 @@ def main():
             run_group([list(reversed(members[0])), list(reversed(members[1]))], lambda i: bwd_ops[i],
                       len(groups) + k)
 
-    def step(ev=None):
-        for i, (_, fn) in enumerate(ops):
-            if ev is not None:
-                ev[i].record()
-            fn()
-        if ev is not None:
-            ev[len(ops)].record()
+    flush_buf = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
 
-    for _ in range(args.warmup):
+    def flush():
+        flush_buf.sum(dtype=torch.int64)
+
+    def step(ev=None, flushed=False):
+        for i, (_, fn) in enumerate(ops):
+            if flushed:
+                flush()
+            if ev is not None:
+                ev[2 * i].record()
+            fn()
+            if ev is not None:
+                ev[2 * i + 1].record()
+
+    for _ in range(warmup):
         step_timed()
     torch.cuda.synchronize()
 
@@ -554,23 +609,22 @@ def main():
     t0 = torch.cuda.Event(enable_timing=True); t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step_timed()
     t1.record()
     torch.cuda.synchronize()
-    ms_per_step = t0.elapsed_time(t1) / args.steps
+    ms_per_step = t0.elapsed_time(t1) / steps
 
     # per-step times: warm (back to back) and with the caches flushed before
     # every step by reading a 1 GiB buffer (L2 and the 256 MB last-level
     # cache then hold that buffer's clean lines, not the step's inputs)
-    nps = min(args.steps, 20)
-    flush_buf = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+    nps = min(steps, 20)
 
-    def per_step(flush):
+    def per_step(flushed):
         evs_ = []
         for _ in range(nps):
-            if flush:
-                flush_buf.sum(dtype=torch.int64)
+            if flushed:
+                flush()
             a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a_.record()
             step_timed()
@@ -584,82 +638,82 @@ def main():
         return {"median": round(q(0.5), 4), "p10": round(q(0.1), 4), "p90": round(q(0.9), 4)}
 
     step_warm, step_flushed = summary(per_step(False)), summary(per_step(True))
-    del flush_buf
-
-    # per-kernel timing: events around each call, same stream (a few steps)
-    psteps = min(args.steps, 20 if len(ops) < 50 else 2)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)] for _ in range(psteps)]
-    for s_ in range(psteps):
-        step(evs[s_])
-    torch.cuda.synchronize()
-    kinds = []
-    for k, _ in ops:
-        if k not in kinds:
-            kinds.append(k)
-    tot_us = {k: 0.0 for k in kinds}
-    calls = {k: 0 for k in kinds}
-    for s_ in range(psteps):
-        for i, (k, _) in enumerate(ops):
-            tot_us[k] += 1e3 * evs[s_][i].elapsed_time(evs[s_][i + 1])
-            calls[k] += 1
-    step_us = {k: tot_us[k] / psteps for k in kinds}          # per step, summed over the step's calls
-    launch_us = {k: tot_us[k] / calls[k] for k in kinds}     # per call
-
     tflops = counts["flops"] / (ms_per_step * 1e-3) / 1e12
-    gemms = [k for k in kinds if k.startswith("gemm")]
-    gemm = max(gemms, key=lambda k: step_us[k])
-    per_call_flops = counts[gemm] / (calls[gemm] / psteps)
-    achieved = counts[gemm] / (step_us[gemm] * 1e-6) / 1e12
-    kname = {"gemm_fwd": "ft::k_gemm_fp4_pipe<false, false, 0, true> (forward)",
-             "gemm_bwd": "ft::k_gemm_fp4_pipe<true, false, 0, true> (backward-input)",
-             "gemm_fwd_gelu": "ft::k_gemm_fp4_pipe<false, false, 1, true> (forward, GELU epilogue)",
-             "gemm_bwd_dgelu": "ft::k_gemm_fp4_pipe<true, false, 2, true> (backward-input, dGELU epilogue)"}[gemm]
-    frac = {}
-    for k in kinds:
-        if k.startswith("gemm"):
-            frac[k + "_mxfp4"] = round(counts[k] / (step_us[k] * 1e-6) / 1e12 / MXFP4_PEAK_TFLOPS, 4)
-        else:
-            frac[k + "_hbm"] = round(counts[k] / (step_us[k] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
-
-    out = {
-        "metric": "fused W4A4 linear fwd+bwd TFLOP/s at FLUX 1024^2 shapes; % MXFP4 MFMA peak",
-        "value": round(tflops, 2),
-        "unit": "TFLOP/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+    rec = {
         "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "mxfp4",
-        "data": "synthetic",
-        "config": {"workload": "%s: %s" % (args.workload, WORKLOAD_TEXT[args.workload]),
+        "tflops": round(tflops, 2),
+        "config": {"workload": "%s: %s" % (workload, WORKLOAD_TEXT[workload]),
                    "layers": len(layers), "lora_rank": layers[0][4], "stabilizer_rank": layers[0][5],
                    "outputs": "activations and input gradients bf16; dA, dB fp32", "parallelism": "single GPU"},
         "pct_mxfp4_peak": round(100.0 * tflops / MXFP4_PEAK_TFLOPS, 2),
         "schedule": ("image and text streams of each double block on two HIP streams; per-kernel times on one"
                      if side is not None else "one HIP stream"),
+        "step_ms": {"steps": nps, "warm": step_warm, "flushed": step_flushed,
+                    "flush": "1 GiB read before each step (L2 and last-level cache hold no inputs)",
+                    "flushed_tflops_median": round(counts["flops"] / (step_flushed["median"] * 1e-3) / 1e12, 2)},
+        "_inputs": d,
+    }
+    if not per_kernel:
+        del flush_buf
+        return rec
+
+    # per-kernel timing: events around each call, same stream, warm (calls
+    # back to back) and flushed (the 1 GiB read before every call, outside
+    # its events: each kernel finds its inputs in HBM only)
+    kinds = []
+    for k, _ in ops:
+        if k not in kinds:
+            kinds.append(k)
+
+    def per_kernel_us(flushed):
+        psteps = min(steps, 20 if len(ops) < 50 else 2)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * len(ops))] for _ in range(psteps)]
+        for s_ in range(psteps):
+            step(evs[s_], flushed)
+        torch.cuda.synchronize()
+        tot_us = {k: 0.0 for k in kinds}
+        calls = {k: 0 for k in kinds}
+        for s_ in range(psteps):
+            for i, (k, _) in enumerate(ops):
+                tot_us[k] += 1e3 * evs[s_][2 * i].elapsed_time(evs[s_][2 * i + 1])
+                calls[k] += 1
+        return {k: tot_us[k] / psteps for k in kinds}, {k: tot_us[k] / calls[k] for k in kinds}, \
+            {k: calls[k] / psteps for k in kinds}
+
+    step_us, launch_us, calls_per_step = per_kernel_us(False)
+    step_us_fl, _, _ = per_kernel_us(True)
+    del flush_buf
+
+    def fracs(us):
+        frac = {}
+        for k in kinds:
+            if k.startswith("gemm"):
+                frac[k + "_mxfp4"] = round(counts[k] / (us[k] * 1e-6) / 1e12 / MXFP4_PEAK_TFLOPS, 4)
+            else:
+                frac[k + "_hbm"] = round(counts[k] / (us[k] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        return frac
+
+    gemms = [k for k in kinds if k.startswith("gemm")]
+    gemm = max(gemms, key=lambda k: step_us[k])
+    per_call_flops = counts[gemm] / calls_per_step[gemm]
+    achieved = counts[gemm] / (step_us[gemm] * 1e-6) / 1e12
+    kname = {"gemm_fwd": "ft::k_gemm_fp4_pipe<false, false, 0, true> (forward)",
+             "gemm_bwd": "ft::k_gemm_fp4_pipe<true, false, 0, true> (backward-input)",
+             "gemm_fwd_gelu": "ft::k_gemm_fp4_pipe<false, false, 1, true> (forward, GELU epilogue)",
+             "gemm_bwd_dgelu": "ft::k_gemm_fp4_pipe<true, false, 2, true> (backward-input, dGELU epilogue)"}[gemm]
+    rec.update({
         "roofline": {"bound": "mfma", "kernel": kname,
                      "achieved": round(achieved, 1), "peak": MXFP4_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / MXFP4_PEAK_TFLOPS, 4),
                      "traffic": measured_traffic("bwd" if gemm == "gemm_bwd" else "fwd")
-                     if args.workload == "flux_qkv" else None,
+                     if workload == "flux_qkv" else None,
                      "per_launch_flops": per_call_flops, "avg_launch_us": round(launch_us[gemm], 2)},
-        "step_ms": {"steps": nps, "warm": step_warm, "flushed": step_flushed,
-                    "flush": "1 GiB read before each step (L2 and last-level cache hold no inputs)",
-                    "flushed_tflops_median": round(counts["flops"] / (step_flushed["median"] * 1e-3) / 1e12, 2)},
         "kernels_us": {k: round(step_us[k], 2) for k in kinds},
-        "kernels_frac": frac,
-    }
-    if not args.no_cpu_baseline:
-        if d is None:
-            shape = gen.SHAPES["flux_qkv"]
-            d = gen.layer_inputs_torch(shape, args.seed, dev)
-        out["cpu_baseline"] = cpu_baseline(d, gen.SHAPES["flux_qkv"], args.cpu_rows)
-        if args.workload != "flux_qkv":
-            out["cpu_baseline"]["sample"] += " (the QKV linear, the oracle's per-linear rate)"
-    print(json.dumps(out), flush=True)
+        "kernels_frac": fracs(step_us),
+        "kernels_us_flushed": {k: round(step_us_fl[k], 2) for k in kinds},
+        "kernels_frac_flushed": fracs(step_us_fl),
+    })
+    return rec
 
 
 def cpu_baseline(d, shape, rows):
