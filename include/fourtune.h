@@ -223,6 +223,25 @@ ft_status ft_lora_grads(const void *x, int64_t M, int64_t K, const void *dy, int
 /* Workspace bytes ft_lora_grads needs for these arguments (0: none). */
 size_t ft_lora_grads_workspace_size(int64_t M, int64_t K, int64_t N, int64_t ld, int32_t r);
 
+/*
+ * ft_lora_grads without a workspace, for callers that cannot allocate device
+ * memory around the call (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Arguments, results and errors are those
+ * of ft_lora_grads; the results are bit-identical to it (same kernels, same
+ * summation order).  The token-chunk partial sums go to a static 32 MiB
+ * device array inside the library instead of a workspace: each GPU the
+ * library runs on holds one until the process ends, and its address is looked
+ * up on the first call on that device (the device current at the call).
+ * Every size this layer accepts fits (the partials never exceed 32 MiB);
+ * sizes that would need more return FT_ERR_UNSUPPORTED.  Nothing is
+ * allocated, freed or synchronized.  All calls on one GPU share the array:
+ * calls that overlap in time on the same GPU (different streams, threads or
+ * processes' graphs replayed concurrently) race and give undefined results.
+ */
+ft_status ft_lora_grads_noalloc(const void *x, int64_t M, int64_t K, const void *dy, int64_t N,
+                                const float *xa, const float *dyb, int64_t ld, int32_t r,
+                                float *dA, float *dB, int32_t accumulate, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *ft_status_string(ft_status status);
 

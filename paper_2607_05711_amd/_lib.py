@@ -61,6 +61,8 @@ def load():
         L.ft_linear_fwd.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P, _P, ctypes.c_int, _P]
         L.ft_linear_bwd_input.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P, ctypes.c_int, _P]
         L.ft_lora_grads.argtypes = [_P, _I64, _I64, _P, _I64, _P, _P, _I64, _I32, _P, _P, _I32, _P, _Z, _P]
+        L.ft_lora_grads_noalloc.argtypes = [_P, _I64, _I64, _P, _I64, _P, _P, _I64, _I32, _P, _P, _I32, _P]
+        L.ft_lora_grads_noalloc.restype = ctypes.c_int
         L.ft_lora_grads_workspace_size.argtypes = [_I64, _I64, _I64, _I64, _I32]
         L.ft_lora_grads_workspace_size.restype = _Z
         L.ft_linear_fwd_gelu.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P,
@@ -384,4 +386,33 @@ def ft_lora_grads(x, dy, xa, dyb, r, col0=0, dA=None, dB=None, accumulate=False,
     _check(L.ft_lora_grads(_ptr(x), M, K, _ptr(dy), N, _ptr(xa, col0), _ptr(dyb, col0), ld, r,
                            _ptr(dA), _ptr(dB), 1 if accumulate else 0, _ptr(workspace), _nbytes(workspace),
                            _stream(dev)))
+    return dA, dB
+
+
+def ft_lora_grads_noalloc(x, dy, xa, dyb, r, col0=0, dA=None, dB=None, accumulate=False):
+    """ft_lora_grads without a workspace: the library's static device scratch
+    holds the token-chunk partials (for callers that cannot allocate around
+    the call; pass dA and dB to allocate nothing here either).  Calls that
+    overlap on one GPU race on that scratch."""
+    L = load()
+    dev = x.device
+    _need(x, "x", torch.bfloat16, ndim=2)
+    _need(dy, "dy", torch.bfloat16, dev, ndim=2)
+    _need(xa, "xa", torch.float32, dev, ndim=2)
+    _need(dyb, "dyb", torch.float32, dev, ndim=2)
+    M, K = x.shape
+    N = dy.shape[1]
+    ld = xa.shape[1]
+    if dy.shape[0] != M or xa.shape[0] != M or dyb.shape != xa.shape or col0 + r > ld:
+        raise ValueError("x [M,K], dy [M,N], xa/dyb [M,ld] shapes mismatch")
+    if dA is None:
+        dA = torch.empty((K, r), dtype=torch.float32, device=dev)
+    if dB is None:
+        dB = torch.empty((r, N), dtype=torch.float32, device=dev)
+    _need(dA, "dA", torch.float32, dev)
+    _need(dB, "dB", torch.float32, dev)
+    if dA.shape != (K, r) or dB.shape != (r, N):
+        raise ValueError("dA must be [K, r] and dB [r, N]")
+    _check(L.ft_lora_grads_noalloc(_ptr(x), M, K, _ptr(dy), N, _ptr(xa, col0), _ptr(dyb, col0), ld, r,
+                                   _ptr(dA), _ptr(dB), 1 if accumulate else 0, _stream(dev)))
     return dA, dB

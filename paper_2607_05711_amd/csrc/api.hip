@@ -222,27 +222,58 @@ size_t ft_lora_grads_workspace_size(int64_t M, int64_t K, int64_t N, int64_t ld,
   return ft::lora_grads_workspace((int)M, (int)K, (int)N, (int)ld, r);
 }
 
-ft_status ft_lora_grads(const void* x, int64_t M, int64_t K, const void* dy, int64_t N, const float* xa,
-                        const float* dyb, int64_t ld, int32_t r, float* dA, float* dB, int32_t accumulate,
-                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  g_last_error[0] = 0;
+static ft_status lora_validate(const void* x, int64_t M, int64_t K, const void* dy, int64_t N, const float* xa,
+                               const float* dyb, int64_t ld, int32_t r, float* dA, float* dB, int32_t accumulate,
+                               bool* nothing) {
+  *nothing = false;
   FT_TRY(check_dim("M", M, 1));
   FT_TRY(check_dim("K", K, 32));
   FT_TRY(check_dim("N", N, 32));
   if (r < 1 || r > 128) return fail(FT_ERR_UNSUPPORTED, "r = %d: need 1 <= r <= 128", r);
   if (ld < r || ld % 4 != 0 || ld > 4096) return fail(FT_ERR_SHAPE, "ld = %lld: need r <= ld <= 4096, ld %% 4 == 0", (long long)ld);
   if (accumulate != 0 && accumulate != 1) return fail(FT_ERR_UNSUPPORTED, "accumulate = %d", accumulate);
-  if (K == 0 && N == 0) return FT_OK;   // dA [0, r] and dB [r, 0] hold nothing
+  if (K == 0 && N == 0) {   // dA [0, r] and dB [r, 0] hold nothing
+    *nothing = true;
+    return FT_OK;
+  }
   if (!dA || !dB) return fail(FT_ERR_NULL, "dA and dB are required");
   if (M > 0 && (!x || !dy || !xa || !dyb)) return fail(FT_ERR_NULL, "x, dy, xa and dyb are required");
   if (K > (1 << 24) || N > (1 << 24)) return fail(FT_ERR_UNSUPPORTED, "K and N above 2^24 are not supported here");
   if ((x && !aligned16(x)) || (dy && !aligned16(dy)) || (xa && !aligned16(xa)) || (dyb && !aligned16(dyb)) ||
       !aligned16(dA) || !aligned16(dB))
     return fail(FT_ERR_ALIGN, "x, dy, xa, dyb, dA, dB must be 16-byte aligned");
+  return FT_OK;
+}
+
+ft_status ft_lora_grads(const void* x, int64_t M, int64_t K, const void* dy, int64_t N, const float* xa,
+                        const float* dyb, int64_t ld, int32_t r, float* dA, float* dB, int32_t accumulate,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  bool nothing;
+  FT_TRY(lora_validate(x, M, K, dy, N, xa, dyb, ld, r, dA, dB, accumulate, &nothing));
+  if (nothing) return FT_OK;
   FT_TRY(check_workspace(workspace, workspace_bytes, ft::lora_grads_workspace((int)M, (int)K, (int)N, (int)ld, r)));
   return hip_status(ft::launch_lora_grads((const uint16_t*)x, (int)M, (int)K, (const uint16_t*)dy, (int)N, xa, dyb,
                                           (int)ld, r, dA, dB, accumulate != 0, (float*)workspace, stream),
                     "lora grads");
+}
+
+ft_status ft_lora_grads_noalloc(const void* x, int64_t M, int64_t K, const void* dy, int64_t N, const float* xa,
+                                const float* dyb, int64_t ld, int32_t r, float* dA, float* dB, int32_t accumulate,
+                                hipStream_t stream) {
+  g_last_error[0] = 0;
+  bool nothing;
+  FT_TRY(lora_validate(x, M, K, dy, N, xa, dyb, ld, r, dA, dB, accumulate, &nothing));
+  if (nothing) return FT_OK;
+  const size_t need = ft::lora_grads_workspace((int)M, (int)K, (int)N, (int)ld, r);
+  if (need > ft::kLoraScratchBytes)
+    return fail(FT_ERR_UNSUPPORTED, "these sizes need %zu bytes of scratch, more than the %zu of the allocation-free "
+                "entry point; call ft_lora_grads with a workspace", need, ft::kLoraScratchBytes);
+  float* scratch = nullptr;
+  if (need > 0) FT_TRY(hip_status(ft::lora_grads_scratch(&scratch), "lora grads scratch lookup"));
+  return hip_status(ft::launch_lora_grads((const uint16_t*)x, (int)M, (int)K, (const uint16_t*)dy, (int)N, xa, dyb,
+                                          (int)ld, r, dA, dB, accumulate != 0, scratch, stream),
+                    "lora grads (no allocation)");
 }
 
 }  // extern "C"

@@ -52,4 +52,11 @@ hipError_t launch_lora_grads(const uint16_t* x, int M, int K, const uint16_t* dy
                              const float* dyb, int ld, int r, float* dA, float* dB, bool accumulate, float* ws,
                              hipStream_t st);
 
+// Size of the static device scratch the allocation-free adapter-gradient entry
+// point uses in place of a workspace, and its device address on the current
+// device (looked up on the first call per device).  Every call on one device
+// shares it.
+constexpr size_t kLoraScratchBytes = (size_t)32 << 20;
+hipError_t lora_grads_scratch(float** ptr);
+
 }  // namespace ft

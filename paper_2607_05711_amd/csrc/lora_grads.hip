@@ -16,6 +16,8 @@
 // odd rows of a 16-row step, which keeps the 32-bit L reads conflict-free.
 // dB's tile has j on the MFMA rows (A = L) and dA's has j on the columns
 // (B = L), so both store contiguous runs in their output layout.
+#include <mutex>
+
 #include "ft_device.h"
 #include "ft_kernels.h"
 
@@ -279,6 +281,38 @@ hipError_t launch_lora_grads(const uint16_t* x, int M, int K, const uint16_t* dy
     if (e == hipSuccess && parts) e = launch_reduce_parts(parts, nmch, (size_t)r * N, dB, (size_t)K * r, dA, acc, st);
     if (e != hipSuccess) return e;
   }
+  return hipSuccess;
+}
+
+// ------------------------------------------------ allocation-free variant
+// Scratch for callers that cannot allocate (code under graph capture, tight
+// serving loops): the token-chunk partials live in this file-scope array,
+// which every GPU the library runs on holds until the process ends.  Host
+// code never passes `scratch` itself (its host-side name is not a device
+// address): the device address comes from hipGetSymbolAddress, looked up once
+// per device with that device current and kept per device.
+static __device__ __align__(256) float scratch[kLoraScratchBytes / sizeof(float)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t lora_grads_scratch(float** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = (float*)p;
+  }
+  *ptr = g_scratch_ptr[dev];
   return hipSuccess;
 }
 

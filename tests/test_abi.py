@@ -203,3 +203,19 @@ def test_load_refuses_a_library_built_from_other_sources(monkeypatch):
     monkeypatch.setattr(build, "source_hash", lambda: "0" * 64)
     with pytest.raises(RuntimeError, match="not built from the sources"):
         _lib.load()
+
+
+def test_lora_noalloc_validation():
+    """The allocation-free adapter-gradient entry point validates like
+    ft_lora_grads (no workspace arguments)."""
+    f = _lib.load().ft_lora_grads_noalloc
+    args = lambda **kw: [kw.get("x", ALIGNED), kw.get("M", 8), kw.get("K", 64), kw.get("dy", ALIGNED), kw.get("N", 64),
+                         kw.get("xa", ALIGNED2), kw.get("dyb", ALIGNED2), kw.get("ld", 32), kw.get("r", 16),
+                         kw.get("dA", ALIGNED), kw.get("dB", ALIGNED), kw.get("acc", 0), NULL]
+    assert f(*args(r=0)) == _lib.FT_ERR_UNSUPPORTED
+    assert f(*args(ld=33)) == _lib.FT_ERR_SHAPE
+    assert f(*args(K=40)) == _lib.FT_ERR_SHAPE
+    assert f(*args(acc=2)) == _lib.FT_ERR_UNSUPPORTED
+    assert f(*args(dB=NULL)) == _lib.FT_ERR_NULL
+    assert f(*args(xa=MISALIGNED)) == _lib.FT_ERR_ALIGN
+    assert f(*args(K=0, N=0, dA=NULL, dB=NULL)) == _lib.FT_OK
