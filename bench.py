@@ -355,14 +355,66 @@ def fusion_ablation(torch, L, d, wq, ws, shape, steps, warmup):
         torch.cuda.synchronize()
         return a.elapsed_time(b) / steps
 
+    bf16_step = bf16_lora_linear(torch, d["W"], d["D"][:, rs:].contiguous(), d["U"][rs:].contiguous(), bias, X, dY)
     tf, tu = timed(fused), timed(unfused)
+    tb = timed(bf16_step)
     tf2 = timed(fused)
     tf = min(tf, tf2)
-    return {"metric": "layer step time, low-rank fusion ablation (flux_qkv)", "unit": "ms",
+    return {"metric": "layer step time, low-rank fusion ablation and BF16 LoRA (flux_qkv)", "unit": "ms",
             "fused_ms": round(tf, 4), "unfused_ms": round(tu, 4), "fusion_speedup": round(tu / tf, 3),
             "unfused": "quantize without projection; FP4 GEMMs without the low-rank branch; down-, up-projections "
                        "and adapter gradients as separate bf16 library matmuls",
+            "bf16_lora_ms": round(tb, 4), "speedup_vs_bf16_lora": round(tb / tf, 3),
+            "bf16_lora": BF16_LORA_TEXT,
             "steps": steps, "warmup": warmup, "data": "synthetic"}
+
+
+BF16_LORA_TEXT = ("16-bit LoRA (W16A16G16): bf16 weight, activations and gradients; the weight and adapter "
+                  "products as bf16 library matmuls (hipBLASLt through torch) with fp32 accumulation, no stabilizer; "
+                  "forward, input gradient and adapter gradients")
+
+
+def bf16_lora_linear(torch, W, A, B, bias, X, dY):
+    """One step of the 16-bit LoRA linear the paper compares against (BF16
+    LoRA): Y = X W^T + bias + (X A) B, then dX = dY W + (dY B^T) A^T,
+    dA = X^T (dY B^T), dB = (X A)^T dY, all bf16 matmuls with fp32
+    accumulation.  The frozen weight is kept in both layouts so that no
+    product takes a transposed right operand."""
+    Wt = W.t().contiguous()                    # [K, N]
+
+    def step():
+        XA = torch.mm(X, A)                    # [M, r]
+        torch.addmm(bias, X, Wt).addmm_(XA, B)
+        G_Bt = torch.mm(dY, B.t().contiguous())    # [M, r]
+        torch.mm(dY, W).addmm_(G_Bt, A.t().contiguous())
+        torch.mm(X.t(), G_Bt)                  # dA [K, r]
+        torch.mm(XA.t(), dY)                   # dB [r, N]
+    return step
+
+
+def bf16_lora_mlp(torch, W1, A1, B1, b1, W2, A2, B2, b2, X, dY):
+    """The MLP pair as 16-bit LoRA: z = X W1^T + b1 + (X A1) B1, h = GELU(z),
+    y = h W2^T + b2 + (h A2) B2, and the backward through both linears and
+    the GELU, with the four adapter gradients."""
+    W1t, W2t = W1.t().contiguous(), W2.t().contiguous()
+    F = torch.nn.functional
+
+    def step():
+        XA1 = torch.mm(X, A1)
+        z = torch.addmm(b1, X, W1t).addmm_(XA1, B1)
+        h = F.gelu(z, approximate="tanh")
+        hA2 = torch.mm(h, A2)
+        torch.addmm(b2, h, W2t).addmm_(hA2, B2)
+        G_B2t = torch.mm(dY, B2.t().contiguous())
+        dh = torch.mm(dY, W2).addmm_(G_B2t, A2.t().contiguous())
+        torch.mm(h.t(), G_B2t)                 # dA2
+        torch.mm(hA2.t(), dY)                  # dB2
+        dz = torch.ops.aten.gelu_backward(dh, z, approximate="tanh")
+        dz_B1t = torch.mm(dz, B1.t().contiguous())
+        torch.mm(dz, W1).addmm_(dz_B1t, A1.t().contiguous())
+        torch.mm(X.t(), dz_B1t)                # dA1
+        torch.mm(XA1.t(), dz)                  # dB1
+    return step
 
 
 def mlp_ablation(torch, L, dev, seed, steps, warmup, M=4608, Dm=3072, F=12288, r=32, rs=32):
@@ -440,12 +492,18 @@ def mlp_ablation(torch, L, dev, seed, steps, warmup, M=4608, Dm=3072, F=12288, r
         t.cuda.synchronize()
         return a.elapsed_time(b) / steps
 
+    W1b, W2b = nrm((F, Dm), 0.02), nrm((Dm, F), 0.02)
+    bf16_step = bf16_lora_mlp(t, W1b, D1[:, rs:].contiguous(), U1[rs:].contiguous(), b1, W2b,
+                              D2[:, rs:].contiguous(), U2[rs:].contiguous(), b2, X, dY)
     tf, tu = timed(fused), timed(unfused)
+    tb = timed(bf16_step)
     tf = min(tf, timed(fused))
-    return {"metric": "MLP pair step time, MLP fusion ablation (flux_mlp)", "unit": "ms",
+    return {"metric": "MLP pair step time, MLP fusion ablation and BF16 LoRA (flux_mlp)", "unit": "ms",
             "fused_ms": round(tf, 4), "unfused_ms": round(tu, 4), "fusion_speedup": round(tu / tf, 3),
             "unfused": "FC1 and FC2 backward-input as plain GEMMs writing z and dH; GELU-tanh and its derivative "
                        "as library elementwise kernels; h and dz quantized with their projections separately",
+            "bf16_lora_ms": round(tb, 4), "speedup_vs_bf16_lora": round(tb / tf, 3),
+            "bf16_lora": BF16_LORA_TEXT,
             "steps": steps, "warmup": warmup, "data": "synthetic"}
 
 
