@@ -27,6 +27,13 @@
  *   - input gradient, Eq. (3):  dX = DQ(Q(G)) DQ(Q(W)) + G (L1 L2)^T + G (A B)^T
  *   - adapter gradients (Sec. 3.2): dB = (X A)^T G, dA = X^T (G B^T)
  *   - GELU (tanh form) and its derivative for the MLP pair (Sec. 3.3, MLP fusion).
+ *   - Numerics variants of Q(.) where Sec. 3.1 leaves the rule open: the
+ *     no-clip shared exponent (the smallest e with max|v| / 2^e <= 6, so no
+ *     element saturates) and stochastic rounding of the elements (each value
+ *     goes to one of its two neighbouring E2M1 magnitudes with probability
+ *     proportional to its distance from the other), whose random bits come
+ *     from the counter-based generator Philox4x32-10 (Salmon, Moraes, Dror
+ *     and Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011).
  *
  * The two GEMM entry points also return S = sum over terms of |term| per
  * output element, the scale against which floating-point parity is judged.
@@ -99,23 +106,96 @@ static int nearest_magnitude_code(double t)
     return best;
 }
 
+/* Shared exponent under a scale rule.
+ *   rule 0 (floor, the Microscaling rule): floor(log2 amax) - 2; the block
+ *          maximum scales into [4, 8) and values above 6 saturate.
+ *   rule 1 (no clip): the smallest e with amax * 2^-e <= 6, i.e.
+ *          ceil(log2(amax / 6)); the block maximum scales into (3, 6].
+ * Both are clamped to the E8M0 range; a zero block gets -127. */
+static int block_exponent_rule(double amax, int rule)
+{
+    int e = block_exponent(amax);
+    if (rule == 1 && amax != 0.0 && ldexp(amax, -e) > 6.0 && e < 127)
+        e += 1;
+    return e;
+}
+
+/* Stochastic rounding of t >= 0 onto the E2M1 magnitudes.  With lo <= t < hi
+ * the two neighbouring magnitudes, t goes up to hi with probability
+ * (t - lo) / (hi - lo): up exactly when that fraction exceeds (u + 1/2) / 2^16
+ * for a uniform 16-bit integer u.  Magnitudes on the grid stay put; t >= 6
+ * saturates to 6. */
+static int stochastic_magnitude_code(double t, unsigned u)
+{
+    if (t >= 6.0)
+        return 7;
+    int c = 0;
+    while (E2M1_MAGNITUDE[c + 1] <= t)
+        c++;
+    double x = (t - E2M1_MAGNITUDE[c]) / (E2M1_MAGNITUDE[c + 1] - E2M1_MAGNITUDE[c]);
+    return x > ((double)u + 0.5) / 65536.0 ? c + 1 : c;
+}
+
 /* Quantize n values sharing one scale: writes n 4-bit codes (one per byte of
- * codes4) and returns the E8M0 scale code. */
-static int quantize_block(const double *v, int n, uint8_t *codes4)
+ * codes4) and returns the E8M0 scale code.  rounding 0: nearest, ties to the
+ * even code; rounding 1: stochastic with the 16-bit uniforms u[i]. */
+static int quantize_block_ex(const double *v, int n, int rule, int rounding, const uint16_t *u,
+                             uint8_t *codes4)
 {
     double amax = 0.0;
     for (int i = 0; i < n; i++)
         if (fabs(v[i]) > amax)
             amax = fabs(v[i]);
-    int e = block_exponent(amax);
+    int e = block_exponent_rule(amax, rule);
     for (int i = 0; i < n; i++) {
         double t = ldexp(fabs(v[i]), -e);   /* exact: scaling by a power of two */
-        int code = nearest_magnitude_code(t);
+        int code = rounding ? stochastic_magnitude_code(t, u[i]) : nearest_magnitude_code(t);
         if (signbit(v[i]))
             code |= 8;
         codes4[i] = (uint8_t)code;
     }
     return e + 127;
+}
+
+/* --------------------------------------------------------- Philox4x32-10 */
+
+/* The counter-based generator Philox4x32 with 10 rounds (Salmon et al., SC
+ * 2011): each round multiplies counter words 0 and 2 by two fixed odd
+ * constants, and the 64-bit products' high halves, xor-ed with the other two
+ * counter words and the round key, and their low halves form the next
+ * counter; the key grows by two Weyl constants between rounds. */
+void fto_philox4x32_10(const uint32_t *ctr, const uint32_t *key, uint32_t *out)
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; round++) {
+        if (round > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+        uint32_t n1 = (uint32_t)p1;
+        uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        uint32_t n3 = (uint32_t)p0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* The 16-bit uniform of element idx (row-major index in its matrix): one
+ * Philox call covers 8 consecutive elements.  Counter = (idx / 8 as two
+ * words, stream as two words), key = seed; element idx takes half idx % 2 (low
+ * half first) of output word (idx % 8) / 2. */
+unsigned fto_sr_bits(uint64_t seed, uint64_t stream, int64_t idx)
+{
+    uint64_t q = (uint64_t)idx >> 3;
+    uint32_t ctr[4] = {(uint32_t)q, (uint32_t)(q >> 32), (uint32_t)stream, (uint32_t)(stream >> 32)};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t out[4];
+    fto_philox4x32_10(ctr, key, out);
+    return (out[(idx & 7) >> 1] >> (16 * (idx & 1))) & 0xFFFFu;
 }
 
 /* Codes are packed two per byte along a row: element 2i in bits 3:0,
@@ -135,6 +215,9 @@ static int get_code(const uint8_t *codes, int64_t cols, int64_t r, int64_t c)
     return (c & 1) ? (b >> 4) : (b & 0x0F);
 }
 
+int fto_quantize_ex(const uint16_t *src, int64_t rows, int64_t cols, int block_rows, int scale_rule,
+                    int rounding, uint64_t seed, uint64_t stream, uint8_t *codes, uint8_t *scales);
+
 /*
  * Quantize a bf16 matrix src[rows, cols] (row-major).
  *   block_rows == 1 : 1x32 blocks along each row; scales[rows, cols/32]
@@ -145,21 +228,40 @@ static int get_code(const uint8_t *codes, int64_t cols, int64_t r, int64_t c)
 int fto_quantize(const uint16_t *src, int64_t rows, int64_t cols, int block_rows,
                  uint8_t *codes, uint8_t *scales)
 {
+    return fto_quantize_ex(src, rows, cols, block_rows, 0, 0, 0, 0, codes, scales);
+}
+
+/*
+ * fto_quantize with the numerics variants:
+ *   scale_rule 0: floor rule (as fto_quantize);  1: no-clip rule.
+ *   rounding   0: nearest, ties to even (as fto_quantize);  1: stochastic,
+ *              element (r, c) drawing fto_sr_bits(seed, stream, r * cols + c).
+ */
+int fto_quantize_ex(const uint16_t *src, int64_t rows, int64_t cols, int block_rows, int scale_rule,
+                    int rounding, uint64_t seed, uint64_t stream, uint8_t *codes, uint8_t *scales)
+{
     if (cols % 32 != 0 || rows < 0 || (block_rows != 1 && block_rows != 32))
         return -1;
     if (block_rows == 32 && rows % 32 != 0)
+        return -1;
+    if ((scale_rule != 0 && scale_rule != 1) || (rounding != 0 && rounding != 1))
         return -1;
     int64_t nbr = rows / block_rows, nbc = cols / 32;
 #pragma omp parallel for schedule(static)
     for (int64_t br = 0; br < nbr; br++) {
         double v[1024];
+        uint16_t u[1024];
         uint8_t c4[1024];
         for (int64_t bc = 0; bc < nbc; bc++) {
             int n = 0;
             for (int i = 0; i < block_rows; i++)
-                for (int j = 0; j < 32; j++)
-                    v[n++] = bf16_value(src[(br * block_rows + i) * cols + bc * 32 + j]);
-            scales[br * nbc + bc] = (uint8_t)quantize_block(v, n, c4);
+                for (int j = 0; j < 32; j++) {
+                    int64_t r = br * block_rows + i, c = bc * 32 + j;
+                    v[n] = bf16_value(src[r * cols + c]);
+                    u[n] = rounding ? (uint16_t)fto_sr_bits(seed, stream, r * cols + c) : 0;
+                    n++;
+                }
+            scales[br * nbc + bc] = (uint8_t)quantize_block_ex(v, n, scale_rule, rounding, u, c4);
             n = 0;
             for (int i = 0; i < block_rows; i++)
                 for (int j = 0; j < 32; j++)

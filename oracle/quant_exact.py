@@ -10,7 +10,10 @@ Sec. 2.3; block-wise use in Sec. 3.2):
   * an element's code is the number of decision thresholds its scaled
     magnitude passes, where each threshold is the midpoint of two adjacent
     E2M1 magnitudes and a magnitude exactly on a midpoint goes to the side
-    whose code is even -- instead of a nearest-value search.
+    whose code is even -- instead of a nearest-value search;
+  * the no-clip exponent walks down from the top of the E8M0 range while the
+    block maximum still fits 6 * 2^e, instead of correcting the floor rule;
+  * stochastic rounding compares exact fractions, not floating point.
 
 Pure Python loops: use on small inputs only.
 """
@@ -60,29 +63,61 @@ def _floor_log2(x):
     return k
 
 
-def quantize_block(bits_list):
-    """bf16 bit patterns of one block -> (E8M0 code, list of 4-bit codes)."""
+# E2M1 magnitudes in code order, as exact fractions.
+_GRID = [Fraction(0), Fraction(1, 2), Fraction(1), Fraction(3, 2), Fraction(2), Fraction(3), Fraction(4),
+         Fraction(6)]
+
+
+def _no_clip_exponent(amax):
+    """The smallest e in [-127, 127] with amax <= 6 * 2^e, found by walking
+    down from an exponent that satisfies it."""
+    e = 127
+    while e > -127 and amax <= 6 * _pow2(e - 1):
+        e -= 1
+    return e
+
+
+def quantize_block(bits_list, scale_rule=0, uniforms=None):
+    """bf16 bit patterns of one block -> (E8M0 code, list of 4-bit codes).
+
+    scale_rule 0: the floor rule; 1: the no-clip rule (smallest exponent at
+    which the block maximum is not above 6).  uniforms: None for
+    nearest-even rounding, else one 16-bit integer u per element for
+    stochastic rounding: a magnitude strictly between two grid values lo < hi
+    moves up when (t - lo) / (hi - lo) > (2u + 1) / 2^17."""
     vals = [bf16_fraction(b) for b in bits_list]
     amax = max(m for m, _ in vals)
     if amax == 0:
         e = -127
-    else:
+    elif scale_rule == 0:
         e = max(-127, min(127, _floor_log2(amax) - 2))
+    else:
+        e = _no_clip_exponent(amax)
     codes = []
-    for mag, sign in vals:
+    for i, (mag, sign) in enumerate(vals):
         t = mag / _pow2(e)
-        code = 0
-        for thr, tie_up in _THRESHOLDS:
-            if t > thr or (t == thr and tie_up):
+        if uniforms is None:
+            code = 0
+            for thr, tie_up in _THRESHOLDS:
+                if t > thr or (t == thr and tie_up):
+                    code += 1
+        elif t >= 6:
+            code = 7
+        else:
+            code = max(c for c in range(8) if _GRID[c] <= t)
+            if _GRID[code] != t and (t - _GRID[code]) / (_GRID[code + 1] - _GRID[code]) > \
+                    Fraction(2 * int(uniforms[i]) + 1, 1 << 17):
                 code += 1
         codes.append(code | (sign << 3))
     return e + 127, codes
 
 
-def quantize_rows(bits, block_rows=1):
+def quantize_rows(bits, block_rows=1, scale_rule=0, uniforms=None):
     """bits: 2-D list/array of bf16 patterns -> (packed codes, scales) as lists.
 
     Packing: element 2i of a row in bits 3:0 of byte i, element 2i+1 in 7:4.
+    uniforms: None (nearest-even) or a 2-D array of 16-bit integers, one per
+    element (stochastic rounding).
     """
     rows = len(bits)
     cols = len(bits[0])
@@ -92,7 +127,9 @@ def quantize_rows(bits, block_rows=1):
         for bc in range(cols // 32):
             block = [int(bits[br * block_rows + i][bc * 32 + j])
                      for i in range(block_rows) for j in range(32)]
-            s, codes = quantize_block(block)
+            u = None if uniforms is None else [int(uniforms[br * block_rows + i][bc * 32 + j])
+                                               for i in range(block_rows) for j in range(32)]
+            s, codes = quantize_block(block, scale_rule, u)
             scales[br][bc] = s
             n = 0
             for i in range(block_rows):

@@ -41,6 +41,12 @@ def lib():
         L.fto_e8m0_value.argtypes = [ctypes.c_int]
         L.fto_quantize.argtypes = [_ptr, _c_i64, _c_i64, ctypes.c_int, _ptr, _ptr]
         L.fto_dequantize.argtypes = [_ptr, _ptr, _c_i64, _c_i64, ctypes.c_int, _ptr]
+        L.fto_quantize_ex.argtypes = [_ptr, _c_i64, _c_i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      ctypes.c_uint64, ctypes.c_uint64, _ptr, _ptr]
+        L.fto_philox4x32_10.argtypes = [_ptr, _ptr, _ptr]
+        L.fto_philox4x32_10.restype = None
+        L.fto_sr_bits.argtypes = [ctypes.c_uint64, ctypes.c_uint64, _c_i64]
+        L.fto_sr_bits.restype = ctypes.c_uint
         L.fto_proj.argtypes = [_ptr, _c_i64, _c_i64, _ptr, _c_i64, ctypes.c_int, _ptr, _ptr]
         L.fto_linear_fwd.argtypes = [_ptr, _ptr, _c_i64, _c_i64, _ptr, _ptr, _c_i64,
                                      _ptr, _ptr, _c_i64, _ptr, _ptr, _ptr, _ptr]
@@ -55,7 +61,7 @@ def lib():
         L.fto_gelu_vec.argtypes = [_ptr, _c_i64, _ptr, ctypes.c_int]
         L.fto_num_threads.restype = ctypes.c_int
         L.fto_num_threads.argtypes = []
-        for f in ("fto_quantize", "fto_dequantize", "fto_proj", "fto_linear_fwd",
+        for f in ("fto_quantize", "fto_quantize_ex", "fto_dequantize", "fto_proj", "fto_linear_fwd",
                   "fto_linear_bwd_input", "fto_lora_grads"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
@@ -88,6 +94,35 @@ def quantize(src_bits, block_rows=1):
     if rc != 0:
         raise ValueError("fto_quantize: unsupported shape %r / block_rows %d" % (src.shape, block_rows))
     return codes, scales
+
+
+def quantize_ex(src_bits, block_rows=1, scale_rule=0, rounding=0, seed=0, stream=0):
+    """quantize with the numerics variants: scale_rule 0 floor / 1 no-clip;
+    rounding 0 nearest-even / 1 stochastic (Philox4x32-10 bits from seed and
+    stream, element (r, c) of the matrix at counter index r * cols + c)."""
+    src = _c(src_bits, np.uint16)
+    rows, cols = src.shape
+    codes = np.zeros((rows, cols // 2), np.uint8)
+    scales = np.zeros((rows // block_rows, cols // 32), np.uint8)
+    rc = lib().fto_quantize_ex(_p(src), rows, cols, block_rows, scale_rule, rounding, seed, stream,
+                               _p(codes), _p(scales))
+    if rc != 0:
+        raise ValueError("fto_quantize_ex: unsupported arguments")
+    return codes, scales
+
+
+def philox4x32_10(ctr, key):
+    """One Philox4x32-10 block: four 32-bit counter words, two key words."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, np.uint32)
+    lib().fto_philox4x32_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def sr_bits(seed, stream, idx):
+    """The 16-bit uniform the stochastic rounding of element idx draws."""
+    return int(lib().fto_sr_bits(seed, stream, idx))
 
 
 def dequantize(codes, scales, cols, block_rows=1):
