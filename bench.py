@@ -54,6 +54,10 @@ def parse():
     ap.add_argument("--cpu-rows", type=int, default=0, help="token rows in the oracle sample (0: auto)")
     ap.add_argument("--ablation", action="store_true",
                     help="flux_qkv / flux_mlp: time the fused step against an unfused one, print one JSON line, exit")
+    ap.add_argument("--numerics", action="store_true",
+                    help="time the quantizer's numerics variants at the QKV shapes, print one JSON line, exit")
+    ap.add_argument("--stability", action="store_true",
+                    help="run the synthetic gradient-norm stability probe, print one JSON line, exit")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (scales HBM counters), then exit")
     return ap.parse_args()
@@ -507,6 +511,137 @@ def mlp_ablation(torch, L, dev, seed, steps, warmup, M=4608, Dm=3072, F=12288, r
             "steps": steps, "warmup": warmup, "data": "synthetic"}
 
 
+def numerics_timing(torch, L, dev, seed, steps, warmup):
+    """Time the quantizer's numerics variants at the QKV shapes (X 4608 x 3072
+    with its [cols, R] projection; dY 4608 x 9216 with its [R, cols]
+    projection), one HIP stream, events around the calls."""
+    shape = __import__("paper_2607_05711_amd.gen", fromlist=["SHAPES"]).SHAPES["flux_qkv"]
+    from paper_2607_05711_amd import gen
+    d = gen.layer_inputs_torch(shape, seed, dev)
+    M, K, N, R = shape.M, shape.K, shape.N, shape.R
+    u8, f32 = torch.uint8, torch.float32
+    e = lambda sh, dt: torch.empty(sh, dtype=dt, device=dev)
+    out = {}
+    for name, src, proj, layout, cols in (("quantize_x", d["X"], d["D"], L.FT_PROJ_COLS_BY_R, K),
+                                          ("quantize_dy", d["dY"], d["U"], L.FT_PROJ_R_BY_COLS, N)):
+        codes, scales, po = e((M, cols // 2), u8), e((M, cols // 32), u8), e((M, R), f32)
+        ws = e((max(16, L.ft_quantize_workspace_size(M, cols, 1, R, layout)),), u8)
+        nbytes = M * cols * (2 + 0.5 + 1 / 32) + M * R * 4 + cols * R * 2
+        for mode, (rule, rnd) in (("floor_nearest", (0, 0)), ("noclip_nearest", (1, 0)),
+                                  ("floor_stochastic", (0, 1)), ("noclip_stochastic", (1, 1))):
+            fn = lambda: L.ft_quantize_blockwise_mode(src, proj=proj, proj_layout=layout, codes=codes, scales=scales,
+                                                      proj_out=po, workspace=ws, scale_rule=rule, rounding=rnd,
+                                                      seed=seed, stream=1)
+            for _ in range(warmup):
+                fn()
+            torch.cuda.synchronize()
+            a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a_.record()
+            for _ in range(steps):
+                fn()
+            b_.record()
+            torch.cuda.synchronize()
+            us = 1e3 * a_.elapsed_time(b_) / steps
+            out["%s_%s" % (name, mode)] = {"us": round(us, 2), "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    return {"metric": "quantize + fused projection time by numerics variant (flux_qkv shapes)", "unit": "us",
+            "variants": out, "steps": steps, "warmup": warmup, "data": "synthetic"}
+
+
+def stability_probe(torch, L, dev, seed, steps=150, M=4096, K=1024, N=1024, r=16, rs=16, lr=2e-3):
+    """A synthetic gradient-norm stability probe (the paper's stabilizer and
+    precision ablation, Sec. 4.3): LoRA fine-tuning of one triple-branch
+    linear toward a teacher whose weight differs from the frozen one by a
+    low-rank term, with Adam on A and B.  Activations carry 1 % outlier
+    channels x30 and the frozen weight is heavy-tailed, so 4-bit quantization
+    error matters.  Variants: the W4A4G4 layer with the stabilizer (L1 L2 from
+    a rank-rs SVD of the weight's quantization residual), without it,
+    with stochastic rounding of the gradient, with the no-clip scale rule;
+    and an unquantized fp32 reference of the same model.  Per step it records
+    the loss and the Frobenius norms of dA and dB; the JSON line summarizes
+    them against the reference."""
+    t = torch
+    g = t.Generator(device=dev)
+    g.manual_seed(seed)
+    f32, bf = t.float32, t.bfloat16
+    nrm = lambda sh, sd: t.randn(sh, generator=g, device=dev, dtype=f32) * sd
+    # frozen weight: Student-t(3)-like tails
+    z = nrm((N, K), 1.0)
+    chi = sum(nrm((N, K), 1.0) ** 2 for _ in range(3)) / 3.0
+    W0 = (0.02 * z / t.sqrt(chi)).to(bf)
+    delta = nrm((N, 8), 0.05) @ nrm((8, K), 0.05)               # what the adapter should learn
+    W_teacher = W0.float() + delta
+    wq, ws, _ = L.ft_quantize_blockwise(W0, block_rows=32)
+    # dequantized weight (offline set-up of the stabilizer; not the probe's step)
+    lut = t.tensor([0, .5, 1, 1.5, 2, 3, 4, 6, -0., -.5, -1, -1.5, -2, -3, -4, -6], device=dev, dtype=f32)
+    codes = t.stack([wq & 15, wq >> 4], dim=-1).reshape(N, K).long()
+    scale = t.exp2(ws.float() - 127.0).repeat_interleave(32, 0).repeat_interleave(32, 1)
+    Wd = lut[codes] * scale
+    Uv, Sv, Vh = t.linalg.svd((W0.float() - Wd).double(), full_matrices=False)
+    L1 = (Vh[:rs].T * Sv[:rs]).float().to(bf)                    # [K, rs]
+    L2 = Uv[:, :rs].T.float().to(bf)                             # [rs, N]
+
+    def batch(step):
+        gb = t.Generator(device=dev)
+        gb.manual_seed(seed * 7919 + step)
+        x = t.randn((M, K), generator=gb, device=dev, dtype=f32)
+        cols = t.randperm(K, generator=gb, device=dev)[: K // 100]
+        x[:, cols] *= 30.0
+        return x
+
+    def run(variant):
+        stab = variant != "no_stabilizer"
+        A = (nrm((K, r), 1.0) / K ** 0.5).requires_grad_(True)
+        B = t.zeros((r, N), device=dev, dtype=f32, requires_grad=True)
+        opt = t.optim.Adam([A, B], lr=lr)
+        rule = 1 if variant == "no_clip" else 0
+        rnd = 1 if variant == "sr_grad" else 0
+        hist = []
+        for step in range(steps):
+            x = batch(step)
+            xb = x.to(bf)
+            target = x @ W_teacher.T
+            if variant == "fp32_reference":
+                y = x @ W0.float().T + (x @ A) @ B
+                loss = 0.5 * ((y - target) ** 2).sum() / M
+                opt.zero_grad()
+                loss.backward()
+                gA, gB = A.grad, B.grad
+            else:
+                D = (t.cat([L1, A.detach().to(bf)], 1) if stab else A.detach().to(bf)).contiguous()
+                U = (t.cat([L2, B.detach().to(bf)], 0) if stab else B.detach().to(bf)).contiguous()
+                xq, xs, P = L.ft_quantize_blockwise_mode(xb, proj=D, scale_rule=rule)
+                y = L.ft_linear_fwd(xq, xs, wq, ws, K, P, U, None, out_dtype=f32)
+                diff = y - target
+                loss = 0.5 * (diff ** 2).sum() / M
+                dY = (diff / M).to(bf)
+                gq, gs, Qp = L.ft_quantize_blockwise_mode(dY, proj=U, proj_layout=L.FT_PROJ_R_BY_COLS,
+                                                          scale_rule=rule, rounding=rnd, seed=seed, stream=step)
+                dA, dB = L.ft_lora_grads(xb, dY, P, Qp, r, col0=rs if stab else 0)
+                opt.zero_grad()
+                A.grad, B.grad = dA, dB
+                gA, gB = dA, dB
+            hist.append((float(loss.detach()), float(gA.norm()), float(gB.norm())))
+            opt.step()
+        return hist
+
+    variants = ["fp32_reference", "w4a4g4", "no_stabilizer", "sr_grad", "no_clip"]
+    hists = {v: run(v) for v in variants}
+    ref_h = hists["fp32_reference"]
+    summary = {}
+    for v, h in hists.items():
+        gn = [(a ** 2 + b ** 2) ** 0.5 for _, a, b in h]
+        gr = [(a ** 2 + b ** 2) ** 0.5 for _, a, b in ref_h]
+        summary[v] = {"loss": {str(k): round(h[k][0], 6) for k in (0, 10, 50, steps // 2, steps - 1)},
+                      "grad_norm": {str(k): round(gn[k], 6) for k in (0, 10, 50, steps // 2, steps - 1)},
+                      "grad_norm_max_over_min": round(max(gn[1:]) / max(min(gn[1:]), 1e-30), 3),
+                      "grad_norm_rel_dev_vs_reference": round(sum(abs(a / b - 1) for a, b in zip(gn[1:], gr[1:]))
+                                                              / (len(gn) - 1), 4)}
+    return {"metric": "synthetic gradient-norm stability probe (LoRA fine-tuning of one triple-branch linear)",
+            "shape": {"M": M, "K": K, "N": N, "r": r, "r_s": rs}, "steps": steps, "optimizer": "Adam lr %g" % lr,
+            "data": "synthetic: X N(0,1) with 1%% channels x30, heavy-tailed frozen W, teacher W + rank-8 delta",
+            "variants": summary}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -525,6 +660,12 @@ def main():
     _lib.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.numerics:
+        print(json.dumps(numerics_timing(torch, _lib, dev, args.seed, args.steps, args.warmup)), flush=True)
+        return
+    if args.stability:
+        print(json.dumps(stability_probe(torch, _lib, dev, args.seed)), flush=True)
+        return
     if args.ablation and args.workload == "flux_mlp":
         print(json.dumps(mlp_ablation(torch, _lib, dev, args.seed, args.steps, args.warmup)), flush=True)
         return

@@ -108,6 +108,55 @@ size_t ft_quantize_workspace_size(int64_t rows, int64_t cols, int32_t block_rows
                                   ft_proj_layout proj_layout);
 
 /*
+ * Numerics variants of Q(.).  Sec. 3.1 fixes the 4-bit format but not the
+ * quantizer's scale rule or rounding; these options cover the readings the
+ * default (floor rule, nearest-even) leaves out.
+ *   scale_rule  FT_SCALE_FLOOR (default): e = floor(log2 max|v|) - 2, values
+ *               above 6 * 2^e saturate to 6.  FT_SCALE_NO_CLIP: the smallest
+ *               e with max|v| <= 6 * 2^e, so nothing saturates (the scale byte
+ *               may then change when dequantized values are quantized again;
+ *               the values do not).
+ *   rounding    FT_ROUND_NEAREST_EVEN (default), or FT_ROUND_STOCHASTIC: an
+ *               element between two E2M1 magnitudes lo < t < hi (t = |v| / 2^e)
+ *               moves up to hi when (t - lo) / (hi - lo) > (u + 1/2) / 2^16,
+ *               u a 16-bit uniform; values on the grid stay.  u comes from the
+ *               counter-based generator Philox4x32-10 (Salmon, Moraes, Dror,
+ *               Shaw, SC 2011) with key = seed (low word first) and counter =
+ *               (i / 8 as two words, stream as two words), i = row * cols +
+ *               col; element i takes the 16-bit half i % 2 (low half first) of
+ *               output word (i % 8) / 2.  Results depend only on (seed,
+ *               stream, i), never on the launch.  1x32 blocks only.
+ *   seed, stream  the generator's key and stream (e.g. a run seed and the
+ *               training step); ignored with nearest-even rounding.
+ *   scales_per_row  block_rows == 32 only (2-D blocked activations): 1 writes
+ *               the scales as [rows, cols/32], every row of a 32x32 tile
+ *               carrying the tile's code, which is the layout ft_linear_fwd
+ *               and ft_linear_bwd_input read for their left operand.
+ */
+typedef enum ft_scale_rule { FT_SCALE_FLOOR = 0, FT_SCALE_NO_CLIP = 1 } ft_scale_rule;
+typedef enum ft_rounding { FT_ROUND_NEAREST_EVEN = 0, FT_ROUND_STOCHASTIC = 1 } ft_rounding;
+typedef struct ft_quant_mode {
+    int32_t scale_rule;        /* ft_scale_rule */
+    int32_t rounding;          /* ft_rounding */
+    uint64_t seed;
+    uint64_t stream;
+    int32_t scales_per_row;    /* 0 or 1 */
+} ft_quant_mode;
+
+/*
+ * ft_quantize_blockwise with a numerics mode (NULL: the defaults, identical to
+ * ft_quantize_blockwise).  Arguments and errors as ft_quantize_blockwise;
+ * FT_ERR_UNSUPPORTED for an unknown option, stochastic rounding with 32x32
+ * blocks, or scales_per_row with 1x32 blocks.  The fused projection is
+ * unaffected by the mode (it uses the unquantized input).
+ */
+ft_status ft_quantize_blockwise_mode(const void *src, int64_t rows, int64_t cols, int32_t block_rows,
+                                     uint8_t *codes, uint8_t *scales,
+                                     const void *proj, int32_t R, ft_proj_layout proj_layout,
+                                     float *proj_out, void *workspace, size_t workspace_bytes,
+                                     const ft_quant_mode *mode, hipStream_t stream);
+
+/*
  * Forward of the triple-branch linear, Eq. (2), in nn.Linear orientation:
  *   y[m,n] = sum_k DQ(xq)[m,k] DQ(wq)[n,k] + sum_j P[m,j] U[j,n] + bias[n]
  * The 4-bit product runs on block-scaled FP4 MFMA with fp32 accumulation; the

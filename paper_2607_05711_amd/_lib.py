@@ -22,6 +22,16 @@ EXPORTED = ("ft_quantize_blockwise", "ft_linear_fwd", "ft_linear_bwd_input", "ft
             "ft_status_string", "ft_last_error")
 
 
+FT_SCALE_FLOOR, FT_SCALE_NO_CLIP = 0, 1
+FT_ROUND_NEAREST_EVEN, FT_ROUND_STOCHASTIC = 0, 1
+
+
+class QuantMode(ctypes.Structure):
+    """ft_quant_mode: scale rule, rounding, Philox seed and stream, per-row tile scales."""
+    _fields_ = [("scale_rule", ctypes.c_int32), ("rounding", ctypes.c_int32), ("seed", ctypes.c_uint64),
+                ("stream", ctypes.c_uint64), ("scales_per_row", ctypes.c_int32)]
+
+
 class FourTuneError(RuntimeError):
     def __init__(self, status, detail):
         self.status = status
@@ -56,6 +66,9 @@ def load():
         L = ctypes.CDLL(LIB_PATH)
         _Z = ctypes.c_size_t
         L.ft_quantize_blockwise.argtypes = [_P, _I64, _I64, _I32, _P, _P, _P, _I32, ctypes.c_int, _P, _P, _Z, _P]
+        L.ft_quantize_blockwise_mode.argtypes = [_P, _I64, _I64, _I32, _P, _P, _P, _I32, ctypes.c_int, _P, _P, _Z,
+                                                 ctypes.POINTER(QuantMode), _P]
+        L.ft_quantize_blockwise_mode.restype = ctypes.c_int
         L.ft_quantize_workspace_size.argtypes = [_I64, _I64, _I32, _I32, ctypes.c_int]
         L.ft_quantize_workspace_size.restype = _Z
         L.ft_linear_fwd.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P, _P, ctypes.c_int, _P]
@@ -143,17 +156,32 @@ def ft_quantize_blockwise(src, block_rows=1, proj=None, proj_layout=FT_PROJ_COLS
     `workspace` (device tensor) holds the projection's partial sums; one of the
     size ft_quantize_workspace_size reports is made when it is not given.
     """
+    return _quantize(src, block_rows, proj, proj_layout, codes, scales, proj_out, workspace, None)
+
+
+def ft_quantize_blockwise_mode(src, block_rows=1, proj=None, proj_layout=FT_PROJ_COLS_BY_R, codes=None,
+                               scales=None, proj_out=None, workspace=None, scale_rule=FT_SCALE_FLOOR,
+                               rounding=FT_ROUND_NEAREST_EVEN, seed=0, stream=0, scales_per_row=False):
+    """ft_quantize_blockwise with the numerics variants (no-clip scale rule,
+    stochastic rounding keyed by (seed, stream), per-row tile scales for 2-D
+    blocked activations)."""
+    mode = QuantMode(scale_rule, rounding, seed, stream, 1 if scales_per_row else 0)
+    return _quantize(src, block_rows, proj, proj_layout, codes, scales, proj_out, workspace, mode)
+
+
+def _quantize(src, block_rows, proj, proj_layout, codes, scales, proj_out, workspace, mode):
     L = load()
     _need(src, "src", torch.bfloat16, ndim=2)
     dev = src.device
     rows, cols = src.shape
+    srows = rows if (mode is not None and mode.scales_per_row) else rows // block_rows
     if codes is None:
         codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=dev)
     if scales is None:
-        scales = torch.empty((rows // block_rows, cols // 32), dtype=torch.uint8, device=dev)
+        scales = torch.empty((srows, cols // 32), dtype=torch.uint8, device=dev)
     _need(codes, "codes", torch.uint8, dev)
     _need(scales, "scales", torch.uint8, dev)
-    if codes.numel() * 2 != rows * cols or scales.numel() * 32 * block_rows != rows * cols:
+    if codes.numel() * 2 != rows * cols or scales.numel() * 32 != srows * cols:
         raise ValueError("codes/scales size does not match src %s with block_rows %d" % (tuple(src.shape), block_rows))
     R = 0
     if proj is not None:
@@ -170,9 +198,14 @@ def ft_quantize_blockwise(src, block_rows=1, proj=None, proj_layout=FT_PROJ_COLS
     else:
         proj_out = None
     workspace = _workspace(L.ft_quantize_workspace_size(rows, cols, block_rows, R, proj_layout), dev, workspace)
-    _check(L.ft_quantize_blockwise(_ptr(src), rows, cols, block_rows, _ptr(codes), _ptr(scales),
-                                   _ptr(proj), R, proj_layout, _ptr(proj_out), _ptr(workspace), _nbytes(workspace),
-                                   _stream(dev)))
+    if mode is None:
+        _check(L.ft_quantize_blockwise(_ptr(src), rows, cols, block_rows, _ptr(codes), _ptr(scales),
+                                       _ptr(proj), R, proj_layout, _ptr(proj_out), _ptr(workspace),
+                                       _nbytes(workspace), _stream(dev)))
+    else:
+        _check(L.ft_quantize_blockwise_mode(_ptr(src), rows, cols, block_rows, _ptr(codes), _ptr(scales),
+                                            _ptr(proj), R, proj_layout, _ptr(proj_out), _ptr(workspace),
+                                            _nbytes(workspace), ctypes.byref(mode), _stream(dev)))
     return codes, scales, proj_out
 
 

@@ -83,10 +83,10 @@ size_t ft_quantize_workspace_size(int64_t rows, int64_t cols, int32_t block_rows
   return ft::quant_rows_workspace((int)rows, (int)cols, R, (int)proj_layout);
 }
 
-ft_status ft_quantize_blockwise(const void* src, int64_t rows, int64_t cols, int32_t block_rows, uint8_t* codes,
-                                uint8_t* scales, const void* proj, int32_t R, ft_proj_layout proj_layout,
-                                float* proj_out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  g_last_error[0] = 0;
+static ft_status quantize_impl(const void* src, int64_t rows, int64_t cols, int32_t block_rows, uint8_t* codes,
+                               uint8_t* scales, const void* proj, int32_t R, ft_proj_layout proj_layout,
+                               float* proj_out, void* workspace, size_t workspace_bytes, const ft::QuantMode& qm,
+                               hipStream_t stream) {
   FT_TRY(check_dim("rows", rows, block_rows == 32 ? 32 : 1));
   FT_TRY(check_dim("cols", cols, 32));
   if (block_rows != 1 && block_rows != 32) return fail(FT_ERR_UNSUPPORTED, "block_rows = %d (1 or 32)", block_rows);
@@ -99,15 +99,48 @@ ft_status ft_quantize_blockwise(const void* src, int64_t rows, int64_t cols, int
   FT_TRY(check_rank(R, proj, proj_out, "proj", "proj_out"));
   if (block_rows == 32) {
     if (R != 0) return fail(FT_ERR_UNSUPPORTED, "projection is only fused with 1x32 blocks");
-    return hip_status(ft::launch_quant_tiles((const uint16_t*)src, (int)rows, (int)cols, codes, scales, stream),
+    if (qm.stochastic) return fail(FT_ERR_UNSUPPORTED, "stochastic rounding is only offered for 1x32 blocks");
+    return hip_status(ft::launch_quant_tiles((const uint16_t*)src, (int)rows, (int)cols, codes, scales, stream, qm),
                       "quantize 32x32");
   }
+  if (qm.scales_per_row) return fail(FT_ERR_UNSUPPORTED, "scales_per_row applies to 32x32 blocks");
   FT_TRY(check_workspace(workspace, workspace_bytes,
                          R ? ft::quant_rows_workspace((int)rows, (int)cols, R, (int)proj_layout) : 0));
   return hip_status(ft::launch_quant_rows((const uint16_t*)src, (int)rows, (int)cols, codes, scales,
                                           (const uint16_t*)proj, R, (int)proj_layout, proj_out, (float*)workspace,
-                                          stream),
+                                          stream, qm),
                     "quantize 1x32");
+}
+
+ft_status ft_quantize_blockwise(const void* src, int64_t rows, int64_t cols, int32_t block_rows, uint8_t* codes,
+                                uint8_t* scales, const void* proj, int32_t R, ft_proj_layout proj_layout,
+                                float* proj_out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  return quantize_impl(src, rows, cols, block_rows, codes, scales, proj, R, proj_layout, proj_out, workspace,
+                       workspace_bytes, ft::QuantMode{}, stream);
+}
+
+ft_status ft_quantize_blockwise_mode(const void* src, int64_t rows, int64_t cols, int32_t block_rows,
+                                     uint8_t* codes, uint8_t* scales, const void* proj, int32_t R,
+                                     ft_proj_layout proj_layout, float* proj_out, void* workspace,
+                                     size_t workspace_bytes, const ft_quant_mode* mode, hipStream_t stream) {
+  g_last_error[0] = 0;
+  ft::QuantMode qm;
+  if (mode) {
+    if (mode->scale_rule != FT_SCALE_FLOOR && mode->scale_rule != FT_SCALE_NO_CLIP)
+      return fail(FT_ERR_UNSUPPORTED, "scale_rule = %d", (int)mode->scale_rule);
+    if (mode->rounding != FT_ROUND_NEAREST_EVEN && mode->rounding != FT_ROUND_STOCHASTIC)
+      return fail(FT_ERR_UNSUPPORTED, "rounding = %d", (int)mode->rounding);
+    if (mode->scales_per_row != 0 && mode->scales_per_row != 1)
+      return fail(FT_ERR_UNSUPPORTED, "scales_per_row = %d", (int)mode->scales_per_row);
+    qm.no_clip = mode->scale_rule == FT_SCALE_NO_CLIP;
+    qm.stochastic = mode->rounding == FT_ROUND_STOCHASTIC;
+    qm.seed = mode->seed;
+    qm.stream = mode->stream;
+    qm.scales_per_row = mode->scales_per_row;
+  }
+  return quantize_impl(src, rows, cols, block_rows, codes, scales, proj, R, proj_layout, proj_out, workspace,
+                       workspace_bytes, qm, stream);
 }
 
 ft_status ft_linear_fwd(const uint8_t* xq, const uint8_t* xs, int64_t M, int64_t K, const uint8_t* wq,

@@ -64,6 +64,78 @@ __device__ __forceinline__ uint32_t e8m0_from_amax_bits(uint32_t amax_bits) {
   return e > 0 ? (uint32_t)e : 0u;
 }
 
+// The no-clip variant: the smallest e with amax / 2^e <= 6 (nothing
+// saturates).  With amax = m 2^E, m in [1, 2): e = E - 2 when m <= 1.5
+// (mantissa bits <= 0x40), else E - 1; clamped at code 0.
+__device__ __forceinline__ uint32_t e8m0_noclip_from_amax_bits(uint32_t amax_bits) {
+  int e = (int)((amax_bits >> 7) & 0xFF) - 2 + ((amax_bits & 0x7F) > 0x40 ? 1 : 0);
+  return e > 0 ? (uint32_t)e : 0u;
+}
+
+// Numerics mode of the 1x32 quantizers (a template argument): bit 0 selects
+// the no-clip scale rule, bit 1 stochastic rounding.
+enum { QM_NOCLIP = 1, QM_SR = 2 };
+
+template <int QM>
+__device__ __forceinline__ uint32_t e8m0_of(uint32_t amax_bits) {
+  if constexpr ((QM & QM_NOCLIP) != 0) return e8m0_noclip_from_amax_bits(amax_bits);
+  else return e8m0_from_amax_bits(amax_bits);
+}
+
+// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC 2011): ten rounds of two
+// 32x32->64-bit products of counter words 0 and 2 with fixed odd constants;
+// the high halves xor the other counter words and the round key, the key
+// grows by two Weyl constants per round.
+__device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                              uint32_t k1, uint32_t (&out)[4]) {
+#pragma unroll
+  for (int round = 0; round < 10; round++) {
+    const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+    const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    c0 = hi1 ^ c1 ^ k0;
+    c1 = lo1;
+    c2 = hi0 ^ c3 ^ k1;
+    c3 = lo0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+// Random stream of stochastic rounding: key = seed, counter words 2 and 3 =
+// stream; counter words 0 and 1 = (element index) / 8.
+struct SrKey { uint32_t k0, k1, s0, s1; };
+
+// Stochastic rounding of 8 consecutive bf16 (packed in w, element 2e in the
+// low half of w[e]) to E2M1 with the block's E8M0 code.  rnd[e] holds the
+// 16-bit uniforms of elements 2e (low half) and 2e + 1.  With t = |v| / 2^e
+// between grid values lo <= t < hi, the element moves up to hi when
+// (t - lo) / (hi - lo) > (u + 1/2) / 2^16; every step is exact in fp32
+// (t has 8 significant bits, the grid spacings are powers of two).  t >= 6
+// saturates.  The sign bit is copied.  Returns 8 codes, element 0 in the low
+// nibble.
+__device__ __forceinline__ uint32_t sr_fp4x8(const uint32_t (&w)[4], uint32_t scale_code, const uint32_t (&rnd)[4]) {
+  const float inv = __uint_as_float((254u - scale_code) << 23);   // 2^-e, a normal fp32 for every code <= 253
+  uint32_t o = 0;
+#pragma unroll
+  for (int i = 0; i < 8; i++) {
+    const uint32_t b = (w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+    const uint32_t u = (rnd[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+    const float t = __uint_as_float((b & 0x7FFFu) << 16) * inv;
+    const float t2 = 2.0f * t;
+    const float f2 = floorf(t2), f1 = floorf(t);
+    uint32_t code;
+    float x;
+    if (t < 2.0f) { code = (uint32_t)f2; x = t2 - f2; }
+    else if (t < 4.0f) { code = (uint32_t)f1 + 2u; x = t - f1; }
+    else if (t < 6.0f) { code = 6u; x = (t - 4.0f) * 0.5f; }
+    else { code = 7u; x = 0.0f; }
+    code += x * 65536.0f > (float)u + 0.5f ? 1u : 0u;
+    o |= (code | ((b >> 12) & 8u)) << (4 * i);
+  }
+  return o;
+}
+
 // 2^(code-127) as an fp32 (2^-127 is the subnormal 0x00400000).
 __device__ __forceinline__ float e8m0_to_f32(uint32_t code) {
   return __uint_as_float(code ? (code << 23) : 0x00400000u);

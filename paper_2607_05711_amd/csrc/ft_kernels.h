@@ -10,11 +10,21 @@ namespace ft {
 // span several chunks, each chunk's fp32 projection partial goes to `ws`
 // (quant_rows_workspace bytes) and a reduction kernel sums them into
 // proj_out; otherwise proj_out is written directly and ws is unused.
+// Numerics variants of the quantizers: the no-clip scale rule, stochastic
+// rounding (Philox4x32-10 bits keyed by seed, counter words 2 and 3 = stream),
+// and for 32x32 tiles scales written once per row.
+struct QuantMode {
+  bool no_clip = false;
+  bool stochastic = false;
+  uint64_t seed = 0, stream = 0;
+  int scales_per_row = 0;
+};
 size_t quant_rows_workspace(int rows, int cols, int R, int layout);
 hipError_t launch_quant_rows(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
-                             const uint16_t* proj, int R, int layout, float* proj_out, float* ws, hipStream_t st);
+                             const uint16_t* proj, int R, int layout, float* proj_out, float* ws, hipStream_t st,
+                             const QuantMode& mode = QuantMode{});
 hipError_t launch_quant_tiles(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
-                              hipStream_t st);
+                              hipStream_t st, const QuantMode& mode = QuantMode{});
 
 // out0 (+)= sum of nparts partials [n0 | n1] in ws; likewise out1.  n0, n1 multiples of 4.
 hipError_t launch_reduce_parts(const float* ws, int nparts, size_t n0, float* out0, size_t n1, float* out1,

@@ -56,10 +56,15 @@ __device__ __forceinline__ uint32_t quad_max(uint32_t m) {
 // scales and codes, the scale bytes staged in the wave's LDS rows, and (XT)
 // the step's bf16 values in the wave's projection tile.  EDGE: rows past
 // the end and blocks past the chunk are zeroed and not stored.
-template <bool EDGE, bool XT, class Store>
+// QM: numerics mode (QM_NOCLIP, QM_SR).  With QM_SR, idx0 is the matrix
+// index (row * cols + column) of this lane's first element in group q = 0 and
+// rstep8 = 8 * cols (the next group's rows); one Philox call draws the
+// uniforms of the lane's 8 elements.
+template <bool EDGE, bool XT, int QM = 0, class Store>
 __device__ __forceinline__ void quant_step(const v4i (&x)[4], int rw0, int rows, bool col_ok, int lr, int lc,
                                            int lane, const Store& store, int st, FT_LDS uint8_t* sc,
-                                           int sc_row, FT_LDS uint16_t* xt) {
+                                           int sc_row, FT_LDS uint16_t* xt, const SrKey& key = SrKey{},
+                                           uint64_t idx0 = 0, uint64_t rstep8 = 0) {
 #pragma unroll
   for (int q = 0; q < 4; q++) {
     const int row = rw0 + 8 * q + lr;
@@ -75,13 +80,20 @@ __device__ __forceinline__ void quant_step(const v4i (&x)[4], int rw0, int rows,
                                                __builtin_elementwise_max(p[2], p[3]));
     uint32_t m = max((uint32_t)pm[0], (uint32_t)pm[1]);
     m = quad_max(m);
-    const uint32_t code = e8m0_from_amax_bits(m);
-    const float s = e8m0_to_f32(code);
+    const uint32_t code = e8m0_of<QM>(m);
     uint32_t o = 0;
-    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[0]), s, 0);
-    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[1]), s, 1);
-    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[2]), s, 2);
-    o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[3]), s, 3);
+    if constexpr ((QM & QM_SR) != 0) {
+      const uint64_t blk8 = (idx0 + (uint64_t)q * rstep8) >> 3;
+      uint32_t rnd[4];
+      philox4x32_10((uint32_t)blk8, (uint32_t)(blk8 >> 32), key.s0, key.s1, key.k0, key.k1, rnd);
+      o = sr_fp4x8(w, code, rnd);
+    } else {
+      const float s = e8m0_to_f32(code);
+      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[0]), s, 0);
+      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[1]), s, 1);
+      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[2]), s, 2);
+      o = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o, __builtin_bit_cast(v2bf, w[3]), s, 3);
+    }
     if (ok) store(q, st, o);
     // scale bytes of (row, blocks 2st, 2st+1): the row's first lane takes the
     // second quad's code along (row_shl:4) and writes both
@@ -91,12 +103,13 @@ __device__ __forceinline__ void quant_step(const v4i (&x)[4], int rw0, int rows,
   }
 }
 
-template <int RT, int MODE, int WAVES, int CW>
+template <int RT, int MODE, int WAVES, int CW, int QM>
 __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __restrict__ src, int rows,
                                                                      int cols, uint8_t* __restrict__ codes,
                                                                      uint8_t* __restrict__ scales,
                                                                      const uint16_t* __restrict__ proj, int R,
-                                                                     float* __restrict__ proj_out, float* __restrict__ parts) {
+                                                                     float* __restrict__ proj_out, float* __restrict__ parts,
+                                                                     SrKey key) {
   using L = QuantLds<RT, MODE, WAVES, CW>;
   __shared__ __attribute__((aligned(16))) uint16_t lds[L::HALFWORDS];
   constexpr int NST = CW / 64;     // 64-column steps per chunk
@@ -176,10 +189,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
     const bool col_ok = blk < nblk;
     // interior (every row of the wave and both blocks of the step in range):
     // no masking; the edge path zeroes what lies outside
+    const uint64_t idx0 = (uint64_t)(rw0 + lr) * cols + c0 + 64 * st + lc;
     if (rw0 + 32 > rows || 2 * st + 2 > nblk)
-      quant_step<true, MODE != 0>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt);
+      quant_step<true, MODE != 0, QM>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt, key,
+                                      idx0, 8ull * cols);
     else
-      quant_step<false, MODE != 0>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt);
+      quant_step<false, MODE != 0, QM>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt, key,
+                                       idx0, 8ull * cols);
 
     if constexpr (MODE != 0) {
       const int g16 = lane >> 4, t16 = lane & 15;
@@ -277,12 +293,12 @@ struct QuantFrLds {
   static constexpr int BYTES = WORK + 32 * QF_MAX_BLOCKS;
 };
 
-template <int RT, int WAVES>
+template <int RT, int WAVES, int QM>
 __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __restrict__ src, int rows, int cols,
                                                               uint8_t* __restrict__ codes,
                                                               uint8_t* __restrict__ scales,
                                                               const uint16_t* __restrict__ proj, int R,
-                                                              float* __restrict__ proj_out) {
+                                                              float* __restrict__ proj_out, SrKey key) {
   using L = QuantFrLds<RT, WAVES>;
   __shared__ __attribute__((aligned(16))) uint8_t lds[L::BYTES];
   constexpr int NT = 64 * WAVES;
@@ -346,10 +362,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __
     const int st = step_of(k), c = 64 * st;
     const int blk = 2 * st + (lane >> 2 & 1);
     const bool col_ok = blk < nbc;
+    const uint64_t idx0 = (uint64_t)(row0 + lr) * cols + c + lc;
     if (row0 + 32 > rows || c + 64 > cols)
-      quant_step<true, true>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt);
+      quant_step<true, true, QM>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt, key, idx0,
+                                 8ull * cols);
     else
-      quant_step<false, true>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt);
+      quant_step<false, true, QM>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt, key, idx0,
+                                  8ull * cols);
     // the step's projection rows
 #pragma unroll
     for (int q = 0; q < NP; q++) {
@@ -422,8 +441,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __
 
 // ---------------------------------------------------------------- tiles
 // One wave per 32x32 tile: lane l takes row l/2, columns 16*(l%2) + [0,16).
+// NOCLIP: the no-clip scale rule.  per_row: scales are written as
+// [rows, cols/32], every row of a tile carrying the tile's code (2-D blocked
+// activations in the layout the GEMM reads), else [rows/32, cols/32].
+template <bool NOCLIP>
 __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict__ src, int rows, int cols,
-                                                     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
+                                                     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
+                                                     int per_row) {
   const int lane = threadIdx.x & 63;
   const int tile = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int nbc = cols >> 5;
@@ -442,7 +466,7 @@ __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict_
   }
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
-  const uint32_t code = e8m0_from_amax_bits(m);
+  const uint32_t code = NOCLIP ? e8m0_noclip_from_amax_bits(m) : e8m0_from_amax_bits(m);
   const float s = e8m0_to_f32(code);
   uint32_t o0 = 0, o1 = 0;
   o0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o0, __builtin_bit_cast(v2bf, w[0]), s, 0);
@@ -454,7 +478,11 @@ __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict_
   o1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o1, __builtin_bit_cast(v2bf, w[6]), s, 2);
   o1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(o1, __builtin_bit_cast(v2bf, w[7]), s, 3);
   *(uint2*)(codes + (size_t)row * (cols >> 1) + (col >> 1)) = make_uint2(o0, o1);
-  if (lane == 0) scales[(size_t)tr * nbc + tc] = (uint8_t)code;
+  if (per_row) {
+    if ((lane & 1) == 0) scales[(size_t)row * nbc + tc] = (uint8_t)code;
+  } else if (lane == 0) {
+    scales[(size_t)tr * nbc + tc] = (uint8_t)code;
+  }
 }
 
 // ---------------------------------------------------------------- launchers
@@ -490,56 +518,83 @@ size_t quant_rows_workspace(int rows, int cols, int R, int layout) {
   return chunks > 1 ? (size_t)chunks * rows * R * sizeof(float) : 0;
 }
 
-template <int RT, int MODE, int WAVES, int CW>
+template <int RT, int MODE, int WAVES, int CW, int QM>
 static hipError_t launch_rows_t(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
-                                const uint16_t* proj, int R, float* proj_out, float* ws, hipStream_t st) {
+                                const uint16_t* proj, int R, float* proj_out, float* ws, const SrKey& key,
+                                hipStream_t st) {
   dim3 grid((rows + 32 * WAVES - 1) / (32 * WAVES), (cols + CW - 1) / CW);
   float* parts = MODE != 0 && grid.y > 1 ? ws : nullptr;
-  k_quant_rows<RT, MODE, WAVES, CW><<<grid, 64 * WAVES, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, parts);
+  k_quant_rows<RT, MODE, WAVES, CW, QM><<<grid, 64 * WAVES, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out,
+                                                                     parts, key);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !parts) return e;
   return launch_reduce_parts(parts, (int)grid.y, (size_t)rows * R, proj_out, 0, nullptr, false, st);
 }
 
-hipError_t launch_quant_rows(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
-                             const uint16_t* proj, int R, int layout, float* proj_out, float* ws, hipStream_t st) {
+template <int QM>
+static hipError_t launch_quant_rows_qm(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
+                                       const uint16_t* proj, int R, int layout, float* proj_out, float* ws,
+                                       const SrKey& key, hipStream_t st) {
   if (!proj || R == 0)
-    return launch_rows_t<1, 0, 4, 384>(src, rows, cols, codes, scales, nullptr, 0, nullptr, nullptr, st);
+    return launch_rows_t<1, 0, 4, 384, QM>(src, rows, cols, codes, scales, nullptr, 0, nullptr, nullptr, key, st);
   const int rt = (R + 31) / 32;
   if (quant_full_rows(rows, cols, R, layout)) {
     const unsigned grid = (unsigned)((rows + 31) / 32);
-    if (rt == 1) k_quant_rows_fr<1, 8><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out);
-    else k_quant_rows_fr<2, 8><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out);
+    if (rt == 1) k_quant_rows_fr<1, 8, QM><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, key);
+    else k_quant_rows_fr<2, 8, QM><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, key);
     return hipGetLastError();
   }
+#define FT_ROWS(RT_, MODE_, CW_) \
+  launch_rows_t<RT_, MODE_, 8, CW_, QM>(src, rows, cols, codes, scales, proj, R, proj_out, ws, key, st)
   if (layout == 0) {
     if (quant_chunk_cols(rows, cols, R, layout) == 256) {
       switch (rt) {
-        case 1: return launch_rows_t<1, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-        case 2: return launch_rows_t<2, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-        case 3: return launch_rows_t<3, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-        default: return launch_rows_t<4, 1, 8, 256>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+        case 1: return FT_ROWS(1, 1, 256);
+        case 2: return FT_ROWS(2, 1, 256);
+        case 3: return FT_ROWS(3, 1, 256);
+        default: return FT_ROWS(4, 1, 256);
       }
     }
     switch (rt) {
-      case 1: return launch_rows_t<1, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-      case 2: return launch_rows_t<2, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-      case 3: return launch_rows_t<3, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-      default: return launch_rows_t<4, 1, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+      case 1: return FT_ROWS(1, 1, 384);
+      case 2: return FT_ROWS(2, 1, 384);
+      case 3: return FT_ROWS(3, 1, 384);
+      default: return FT_ROWS(4, 1, 384);
     }
   }
   switch (rt) {
-    case 1: return launch_rows_t<1, 2, 8, 768>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-    case 2: return launch_rows_t<2, 2, 8, 768>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-    case 3: return launch_rows_t<3, 2, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
-    default: return launch_rows_t<4, 2, 8, 384>(src, rows, cols, codes, scales, proj, R, proj_out, ws, st);
+    case 1: return FT_ROWS(1, 2, 768);
+    case 2: return FT_ROWS(2, 2, 768);
+    case 3: return FT_ROWS(3, 2, 384);
+    default: return FT_ROWS(4, 2, 384);
+  }
+#undef FT_ROWS
+}
+
+hipError_t launch_quant_rows(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
+                             const uint16_t* proj, int R, int layout, float* proj_out, float* ws, hipStream_t st,
+                             const QuantMode& mode) {
+  const SrKey key{(uint32_t)mode.seed, (uint32_t)(mode.seed >> 32), (uint32_t)mode.stream,
+                  (uint32_t)(mode.stream >> 32)};
+  switch ((mode.no_clip ? QM_NOCLIP : 0) | (mode.stochastic ? QM_SR : 0)) {
+    case 0: return launch_quant_rows_qm<0>(src, rows, cols, codes, scales, proj, R, layout, proj_out, ws, key, st);
+    case QM_NOCLIP:
+      return launch_quant_rows_qm<QM_NOCLIP>(src, rows, cols, codes, scales, proj, R, layout, proj_out, ws, key, st);
+    case QM_SR:
+      return launch_quant_rows_qm<QM_SR>(src, rows, cols, codes, scales, proj, R, layout, proj_out, ws, key, st);
+    default:
+      return launch_quant_rows_qm<QM_NOCLIP | QM_SR>(src, rows, cols, codes, scales, proj, R, layout, proj_out, ws,
+                                                     key, st);
   }
 }
 
 hipError_t launch_quant_tiles(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
-                              hipStream_t st) {
+                              hipStream_t st, const QuantMode& mode) {
   const int tiles = (rows / 32) * (cols / 32);
-  k_quant_tiles<<<(tiles + 3) / 4, 256, 0, st>>>(src, rows, cols, codes, scales);
+  if (mode.no_clip)
+    k_quant_tiles<true><<<(tiles + 3) / 4, 256, 0, st>>>(src, rows, cols, codes, scales, mode.scales_per_row);
+  else
+    k_quant_tiles<false><<<(tiles + 3) / 4, 256, 0, st>>>(src, rows, cols, codes, scales, mode.scales_per_row);
   return hipGetLastError();
 }
 

@@ -219,3 +219,20 @@ def test_lora_noalloc_validation():
     assert f(*args(dB=NULL)) == _lib.FT_ERR_NULL
     assert f(*args(xa=MISALIGNED)) == _lib.FT_ERR_ALIGN
     assert f(*args(K=0, N=0, dA=NULL, dB=NULL)) == _lib.FT_OK
+
+
+def test_quantize_mode_validation():
+    """ft_quantize_blockwise_mode rejects unknown options and the combinations
+    it does not offer before launching anything."""
+    f = _lib.load().ft_quantize_blockwise_mode
+    M = _lib.QuantMode
+    call = lambda mode, block_rows=1, rows=64: f(ALIGNED, rows, 64, block_rows, ALIGNED, ALIGNED2, NULL, 0, 0,
+                                                 NULL, NULL, 0, ctypes.byref(mode) if mode else None, NULL)
+    assert call(M(2, 0, 0, 0, 0)) == _lib.FT_ERR_UNSUPPORTED                 # scale rule
+    assert call(M(0, 5, 0, 0, 0)) == _lib.FT_ERR_UNSUPPORTED                 # rounding
+    assert call(M(0, 0, 0, 0, 2)) == _lib.FT_ERR_UNSUPPORTED                 # scales_per_row
+    assert call(M(0, 1, 0, 0, 0), block_rows=32) == _lib.FT_ERR_UNSUPPORTED  # stochastic 32x32
+    assert call(M(0, 0, 0, 0, 1), block_rows=1) == _lib.FT_ERR_UNSUPPORTED   # per-row scales of 1x32
+    assert call(M(0, 0, 0, 0, 0), rows=-1) == _lib.FT_ERR_SHAPE
+    assert f(ALIGNED, 64, 64, 1, ALIGNED, MISALIGNED, NULL, 0, 0, NULL, NULL, 0, None, NULL) == _lib.FT_ERR_ALIGN
+    assert f(NULL, 0, 64, 1, NULL, NULL, NULL, 0, 0, NULL, NULL, 0, None, NULL) == _lib.FT_OK
