@@ -34,6 +34,10 @@
  *     proportional to its distance from the other), whose random bits come
  *     from the counter-based generator Philox4x32-10 (Salmon, Moraes, Dror
  *     and Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011).
+ *   - NVFP4 semantics, the format Sec. 3.1 names (NVIDIA's two-level scaling):
+ *     E2M1 elements, one FP8 E4M3 scale per 16 elements (16x16 tiles for the
+ *     weight, Sec. 4.3), and one FP32 scale per tensor; used as an accuracy
+ *     cross-check of the MXFP4 reading.
  *
  * The two GEMM entry points also return S = sum over terms of |term| per
  * output element, the scale against which floating-point parity is judged.
@@ -285,6 +289,139 @@ int fto_dequantize(const uint8_t *codes, const uint8_t *scales, int64_t rows, in
         for (int64_t c = 0; c < cols; c++) {
             int s = scales[(r / block_rows) * nbc + c / 32];
             out[r * cols + c] = fto_e2m1_value(get_code(codes, cols, r, c)) * fto_e8m0_value(s);
+        }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ NVFP4 */
+
+/* Value of an FP8 E4M3 code (OCP 8-bit floating point, E4M3: bias 7, three
+ * mantissa bits, no infinities; exponent and mantissa all ones is NaN).
+ * Exponent field 0 holds the subnormals m/8 * 2^-6. */
+double fto_e4m3_value(int code)
+{
+    int s = (code >> 7) & 1, e = (code >> 3) & 15, m = code & 7;
+    double v;
+    if (e == 15 && m == 7)
+        return NAN;
+    if (e == 0)
+        v = ldexp((double)m / 8.0, -6);
+    else
+        v = ldexp(1.0 + (double)m / 8.0, e - 7);
+    return s ? -v : v;
+}
+
+/* Nearest non-negative E4M3 code to x >= 0 (ties to the even code, i.e. the
+ * even mantissa), saturating at the largest finite value 448 (code 0x7E). */
+static int e4m3_nearest_code(double x)
+{
+    int best = 0;
+    double best_d = fabs(x - fto_e4m3_value(0));
+    for (int c = 1; c <= 0x7E; c++) {
+        double d = fabs(x - fto_e4m3_value(c));
+        if (d < best_d || (d == best_d && (c & 1) == 0)) {
+            best_d = d;
+            best = c;
+        }
+    }
+    return best;
+}
+
+/* NVFP4 tensor scale: the FP32 value amax / (6 * 448) (one correctly rounded
+ * FP32 division), which maps the tensor's largest magnitude onto the largest
+ * block scale times the largest element. */
+float fto_nvfp4_tensor_scale(const uint16_t *src, int64_t n)
+{
+    float amax = 0.0f;
+    for (int64_t i = 0; i < n; i++) {
+        float v = (float)fabs(bf16_value(src[i]));
+        if (v > amax)
+            amax = v;
+    }
+    return amax / 2688.0f;
+}
+
+/*
+ * NVFP4 quantization of a bf16 matrix src[rows, cols] with tensor scale st:
+ *   block_rows 1 : 1x16 blocks along rows; scales[rows, cols/16]
+ *   block_rows 16: 16x16 tiles;            scales[rows/16, cols/16]
+ * Block scale: the E4M3 code nearest to d = amax_b / (6 * st), computed as two
+ * FP32 operations (6 * st, then the division), saturating at 448.  Element:
+ * the nearest E2M1 value to |v| / (E4M3(scale) * st) in exact arithmetic,
+ * ties to the even code, saturating at 6, sign copied; a zero block scale
+ * gives zero codes.  codes[rows, cols/2] packed as fto_quantize.
+ */
+int fto_quantize_nvfp4(const uint16_t *src, int64_t rows, int64_t cols, int block_rows, float st,
+                       uint8_t *codes, uint8_t *scales)
+{
+    if (cols % 16 != 0 || rows < 0 || (block_rows != 1 && block_rows != 16))
+        return -1;
+    if (block_rows == 16 && rows % 16 != 0)
+        return -1;
+    int64_t nbr = rows / block_rows, nbc = cols / 16;
+    const float st6 = 6.0f * st;
+#pragma omp parallel for schedule(static)
+    for (int64_t br = 0; br < nbr; br++)
+        for (int64_t bc = 0; bc < nbc; bc++) {
+            float amax = 0.0f;
+            for (int i = 0; i < block_rows; i++)
+                for (int j = 0; j < 16; j++) {
+                    float v = (float)fabs(bf16_value(src[(br * block_rows + i) * cols + bc * 16 + j]));
+                    if (v > amax)
+                        amax = v;
+                }
+            float d = st6 > 0.0f ? amax / st6 : 0.0f;
+            int sc = e4m3_nearest_code((double)d);
+            scales[br * nbc + bc] = (uint8_t)sc;
+            double bs = fto_e4m3_value(sc) * (double)st;   /* exact: 4 x 24 significant bits */
+            for (int i = 0; i < block_rows; i++)
+                for (int j = 0; j < 16; j++) {
+                    int64_t r = br * block_rows + i, c = bc * 16 + j;
+                    double v = bf16_value(src[r * cols + c]);
+                    int code = bs > 0.0 ? nearest_magnitude_code(fabs(v) / bs) : 0;
+                    if (signbit(v))
+                        code |= 8;
+                    put_code(codes, cols, r, c, code);
+                }
+        }
+    return 0;
+}
+
+/* Dequantize NVFP4 codes/scales (layout as fto_quantize_nvfp4) with tensor
+ * scale st into out[rows, cols]: E2M1 * E4M3 * st, exact in fp64. */
+int fto_dequantize_nvfp4(const uint8_t *codes, const uint8_t *scales, int64_t rows, int64_t cols, int block_rows,
+                         float st, double *out)
+{
+    if (cols % 16 != 0 || (block_rows != 1 && block_rows != 16))
+        return -1;
+    int64_t nbc = cols / 16;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; r++)
+        for (int64_t c = 0; c < cols; c++) {
+            int sc = scales[(r / block_rows) * nbc + c / 16];
+            out[r * cols + c] = fto_e2m1_value(get_code(codes, cols, r, c)) * fto_e4m3_value(sc) * (double)st;
+        }
+    return 0;
+}
+
+/* Product of two dequantized operands, as the forward (trans_b = 1:
+ * y[m,n] = sum_k a[m,k] b[n,k]) or the input gradient (trans_b = 0:
+ * y[m,k] = sum_n a[m,n] b[n,k]); s = sum of |terms|. */
+int fto_gemm_f64(const double *a, const double *b, int64_t M, int64_t N, int64_t K, int trans_b,
+                 double *y, double *s)
+{
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t m = 0; m < M; m++)
+        for (int64_t n = 0; n < N; n++) {
+            double acc = 0.0, mag = 0.0;
+            for (int64_t k = 0; k < K; k++) {
+                double t = a[m * K + k] * (trans_b ? b[n * K + k] : b[k * N + n]);
+                acc += t;
+                mag += fabs(t);
+            }
+            y[m * N + n] = acc;
+            if (s)
+                s[m * N + n] = mag;
         }
     return 0;
 }

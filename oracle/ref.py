@@ -47,6 +47,13 @@ def lib():
         L.fto_philox4x32_10.restype = None
         L.fto_sr_bits.argtypes = [ctypes.c_uint64, ctypes.c_uint64, _c_i64]
         L.fto_sr_bits.restype = ctypes.c_uint
+        L.fto_e4m3_value.restype = ctypes.c_double
+        L.fto_e4m3_value.argtypes = [ctypes.c_int]
+        L.fto_nvfp4_tensor_scale.restype = ctypes.c_float
+        L.fto_nvfp4_tensor_scale.argtypes = [_ptr, _c_i64]
+        L.fto_quantize_nvfp4.argtypes = [_ptr, _c_i64, _c_i64, ctypes.c_int, ctypes.c_float, _ptr, _ptr]
+        L.fto_dequantize_nvfp4.argtypes = [_ptr, _ptr, _c_i64, _c_i64, ctypes.c_int, ctypes.c_float, _ptr]
+        L.fto_gemm_f64.argtypes = [_ptr, _ptr, _c_i64, _c_i64, _c_i64, ctypes.c_int, _ptr, _ptr]
         L.fto_proj.argtypes = [_ptr, _c_i64, _c_i64, _ptr, _c_i64, ctypes.c_int, _ptr, _ptr]
         L.fto_linear_fwd.argtypes = [_ptr, _ptr, _c_i64, _c_i64, _ptr, _ptr, _c_i64,
                                      _ptr, _ptr, _c_i64, _ptr, _ptr, _ptr, _ptr]
@@ -61,7 +68,8 @@ def lib():
         L.fto_gelu_vec.argtypes = [_ptr, _c_i64, _ptr, ctypes.c_int]
         L.fto_num_threads.restype = ctypes.c_int
         L.fto_num_threads.argtypes = []
-        for f in ("fto_quantize", "fto_quantize_ex", "fto_dequantize", "fto_proj", "fto_linear_fwd",
+        for f in ("fto_quantize", "fto_quantize_ex", "fto_dequantize", "fto_quantize_nvfp4", "fto_dequantize_nvfp4",
+                  "fto_gemm_f64", "fto_proj", "fto_linear_fwd",
                   "fto_linear_bwd_input", "fto_lora_grads"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
@@ -123,6 +131,52 @@ def philox4x32_10(ctr, key):
 def sr_bits(seed, stream, idx):
     """The 16-bit uniform the stochastic rounding of element idx draws."""
     return int(lib().fto_sr_bits(seed, stream, idx))
+
+
+def e4m3_value(code):
+    return lib().fto_e4m3_value(int(code))
+
+
+def nvfp4_tensor_scale(src_bits):
+    src = _c(src_bits, np.uint16)
+    return float(np.float32(lib().fto_nvfp4_tensor_scale(_p(src), src.size)))
+
+
+def quantize_nvfp4(src_bits, block_rows=1, tensor_scale=None):
+    """NVFP4: (codes [rows, cols/2], E4M3 scales [rows/block_rows, cols/16],
+    FP32 tensor scale); block_rows 1 (1x16 blocks) or 16 (16x16 tiles)."""
+    src = _c(src_bits, np.uint16)
+    rows, cols = src.shape
+    st = nvfp4_tensor_scale(src) if tensor_scale is None else float(np.float32(tensor_scale))
+    codes = np.zeros((rows, cols // 2), np.uint8)
+    scales = np.zeros((rows // block_rows, cols // 16), np.uint8)
+    rc = lib().fto_quantize_nvfp4(_p(src), rows, cols, block_rows, st, _p(codes), _p(scales))
+    if rc != 0:
+        raise ValueError("fto_quantize_nvfp4: unsupported arguments")
+    return codes, scales, st
+
+
+def dequantize_nvfp4(codes, scales, st, cols, block_rows=1):
+    codes = _c(codes, np.uint8)
+    scales = _c(scales, np.uint8)
+    rows = codes.shape[0]
+    out = np.zeros((rows, cols), np.float64)
+    rc = lib().fto_dequantize_nvfp4(_p(codes), _p(scales), rows, cols, block_rows, float(st), _p(out))
+    if rc != 0:
+        raise ValueError("fto_dequantize_nvfp4: unsupported arguments")
+    return out
+
+
+def gemm_f64(a, b, trans_b=True, want_s=True):
+    """trans_b: y = a b^T (b [N, K]); else y = a b (b [K, N]); with S = sum |terms|."""
+    a = _c(a, np.float64)
+    b = _c(b, np.float64)
+    M, K = a.shape
+    N = b.shape[0] if trans_b else b.shape[1]
+    y = np.zeros((M, N))
+    s = np.zeros((M, N)) if want_s else None
+    lib().fto_gemm_f64(_p(a), _p(b), M, N, K, 1 if trans_b else 0, _p(y), _p(s))
+    return y, s
 
 
 def dequantize(codes, scales, cols, block_rows=1):
