@@ -291,6 +291,46 @@ ft_status ft_lora_grads_noalloc(const void *x, int64_t M, int64_t K, const void 
                                 const float *xa, const float *dyb, int64_t ld, int32_t r,
                                 float *dA, float *dB, int32_t accumulate, hipStream_t stream);
 
+/*
+ * NVFP4 emulation: the 4-bit format Sec. 3.1 names (E2M1 elements, one FP8
+ * E4M3 scale per 16 elements, one FP32 scale per tensor; 16x16 tiles for the
+ * weight, Sec. 4.3), as an accuracy cross-check of the layer's native MXFP4.
+ * gfx950's block-scaled MFMA takes E8M0 scales per 32 elements, so these
+ * calls dequantize to bf16 inside the GEMM (exact: E2M1 x E4M3 has at most 6
+ * significant bits) and run bf16 MFMAs; they are not a fast path.
+ *
+ * ft_quantize_nvfp4:
+ *   src          bf16 [rows, cols]; cols % 16 == 0.
+ *   block_rows   1 (1x16 blocks along rows; scales [rows, cols/16]) or 16
+ *                (16x16 tiles, rows % 16 == 0; scales [rows/16, cols/16]).
+ *   codes        uint8 [rows, cols/2], packed E2M1 as ft_quantize_blockwise.
+ *   scales       uint8 FP8 E4M3 codes (OCP E4M3: bias 7, no infinities).
+ *   tensor_scale one fp32 in device memory, written: st = amax(|src|) / (6 * 448)
+ *                rounded once to fp32.  Used as scratch while the call runs.
+ * Block scale: the E4M3 value nearest to amax_block / (6 st) (the fp32
+ * product 6 st, then the fp32 quotient), ties to the even mantissa,
+ * saturating at 448.  Element: the E2M1 value nearest to |v| / (E4M3 * st)
+ * (exact), ties to the even code, saturating at 6, sign copied; a zero block
+ * scale gives zero codes.
+ */
+ft_status ft_quantize_nvfp4(const void *src, int64_t rows, int64_t cols, int32_t block_rows,
+                            uint8_t *codes, uint8_t *scales, float *tensor_scale, hipStream_t stream);
+
+/*
+ * Forward and input-gradient GEMMs on NVFP4 operands (fp32 outputs):
+ *   y[m,n]  = xt wt sum_k DQ(xq)[m,k] DQ(wq)[n,k]    x: 1x16 blocks along K; w: 16x16 tiles [N, K]
+ *   dx[m,k] = gt wt sum_n DQ(gq)[m,n] DQ(wq)[n,k]    g: 1x16 blocks along N; the same w, read
+ *                                                    transposed with its tile scales (Sec. 3.2)
+ * DQ = E2M1 x E4M3 without the tensor scale; xt, gt, wt: the tensor scales
+ * (device fp32) from ft_quantize_nvfp4.  K and N multiples of 16.
+ */
+ft_status ft_linear_fwd_nvfp4(const uint8_t *xq, const uint8_t *xs, const float *xt, int64_t M, int64_t K,
+                              const uint8_t *wq, const uint8_t *ws, const float *wt, int64_t N,
+                              float *y, hipStream_t stream);
+ft_status ft_linear_bwd_input_nvfp4(const uint8_t *gq, const uint8_t *gs, const float *gt, int64_t M, int64_t N,
+                                    const uint8_t *wq, const uint8_t *ws, const float *wt, int64_t K,
+                                    float *dx, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *ft_status_string(ft_status status);
 

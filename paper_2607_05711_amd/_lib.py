@@ -69,6 +69,12 @@ def load():
         L.ft_quantize_blockwise_mode.argtypes = [_P, _I64, _I64, _I32, _P, _P, _P, _I32, ctypes.c_int, _P, _P, _Z,
                                                  ctypes.POINTER(QuantMode), _P]
         L.ft_quantize_blockwise_mode.restype = ctypes.c_int
+        L.ft_quantize_nvfp4.argtypes = [_P, _I64, _I64, _I32, _P, _P, _P, _P]
+        L.ft_quantize_nvfp4.restype = ctypes.c_int
+        L.ft_linear_fwd_nvfp4.argtypes = [_P, _P, _P, _I64, _I64, _P, _P, _P, _I64, _P, _P]
+        L.ft_linear_fwd_nvfp4.restype = ctypes.c_int
+        L.ft_linear_bwd_input_nvfp4.argtypes = [_P, _P, _P, _I64, _I64, _P, _P, _P, _I64, _P, _P]
+        L.ft_linear_bwd_input_nvfp4.restype = ctypes.c_int
         L.ft_quantize_workspace_size.argtypes = [_I64, _I64, _I32, _I32, ctypes.c_int]
         L.ft_quantize_workspace_size.restype = _Z
         L.ft_linear_fwd.argtypes = [_P, _P, _I64, _I64, _P, _P, _I64, _P, _I32, _P, _P, _P, ctypes.c_int, _P]
@@ -449,3 +455,39 @@ def ft_lora_grads_noalloc(x, dy, xa, dyb, r, col0=0, dA=None, dB=None, accumulat
     _check(L.ft_lora_grads_noalloc(_ptr(x), M, K, _ptr(dy), N, _ptr(xa, col0), _ptr(dyb, col0), ld, r,
                                    _ptr(dA), _ptr(dB), 1 if accumulate else 0, _stream(dev)))
     return dA, dB
+
+
+def ft_quantize_nvfp4(src, block_rows=1):
+    """NVFP4 emulation: (codes uint8 [rows, cols/2], E4M3 scales uint8
+    [rows/block_rows, cols/16], tensor scale fp32 [1]) of bf16 src."""
+    L = load()
+    _need(src, "src", torch.bfloat16, ndim=2)
+    dev = src.device
+    rows, cols = src.shape
+    codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=dev)
+    scales = torch.empty((rows // block_rows, cols // 16), dtype=torch.uint8, device=dev)
+    st = torch.empty((1,), dtype=torch.float32, device=dev)
+    _check(L.ft_quantize_nvfp4(_ptr(src), rows, cols, block_rows, _ptr(codes), _ptr(scales), _ptr(st), _stream(dev)))
+    return codes, scales, st
+
+
+def ft_linear_fwd_nvfp4(xq, xs, xt, wq, ws, wt, K):
+    """y [M, N] fp32 = xt wt DQ(xq) DQ(wq)^T on NVFP4 operands."""
+    L = load()
+    dev = xq.device
+    M, N = xq.shape[0], wq.shape[0]
+    y = torch.empty((M, N), dtype=torch.float32, device=dev)
+    _check(L.ft_linear_fwd_nvfp4(_ptr(xq), _ptr(xs), _ptr(xt), M, K, _ptr(wq), _ptr(ws), _ptr(wt), N, _ptr(y),
+                                 _stream(dev)))
+    return y
+
+
+def ft_linear_bwd_input_nvfp4(gq, gs, gt, wq, ws, wt, K):
+    """dx [M, K] fp32 = gt wt DQ(gq) DQ(wq) on NVFP4 operands (w read transposed)."""
+    L = load()
+    dev = gq.device
+    M, N = gq.shape[0], wq.shape[0]
+    dx = torch.empty((M, K), dtype=torch.float32, device=dev)
+    _check(L.ft_linear_bwd_input_nvfp4(_ptr(gq), _ptr(gs), _ptr(gt), M, N, _ptr(wq), _ptr(ws), _ptr(wt), K, _ptr(dx),
+                                       _stream(dev)))
+    return dx

@@ -309,4 +309,52 @@ ft_status ft_lora_grads_noalloc(const void* x, int64_t M, int64_t K, const void*
                     "lora grads (no allocation)");
 }
 
+ft_status ft_quantize_nvfp4(const void* src, int64_t rows, int64_t cols, int32_t block_rows, uint8_t* codes,
+                            uint8_t* scales, float* tensor_scale, hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (block_rows != 1 && block_rows != 16) return fail(FT_ERR_UNSUPPORTED, "block_rows = %d (1 or 16)", block_rows);
+  FT_TRY(check_dim("rows", rows, block_rows));
+  FT_TRY(check_dim("cols", cols, 16));
+  if (rows == 0 || cols == 0) return FT_OK;
+  if ((rows / 16 + 1) * (cols / 16) >= ((int64_t)1 << 31)) return fail(FT_ERR_SHAPE, "rows * cols too large");
+  if (!src || !codes || !scales || !tensor_scale) return fail(FT_ERR_NULL, "src, codes, scales, tensor_scale are required");
+  if (!aligned16(src) || !aligned16(codes) || !aligned16(scales) || ((uintptr_t)tensor_scale & 3u))
+    return fail(FT_ERR_ALIGN, "src, codes, scales must be 16-byte aligned and tensor_scale 4-byte aligned");
+  return hip_status(ft::launch_quant_nvfp4((const uint16_t*)src, (int)rows, (int)cols, block_rows, codes, scales,
+                                           tensor_scale, stream),
+                    "quantize nvfp4");
+}
+
+static ft_status nvfp4_gemm(bool bwd, const uint8_t* a, const uint8_t* as, const float* at, int64_t M, int64_t KR,
+                            const uint8_t* wq, const uint8_t* ws, const float* wt, int64_t NO, float* out,
+                            hipStream_t stream) {
+  FT_TRY(check_dim("M", M, 1));
+  FT_TRY(check_dim(bwd ? "N" : "K", KR, 16));
+  FT_TRY(check_dim(bwd ? "K" : "N", NO, 16));
+  if (M == 0 || NO == 0) return FT_OK;
+  if (KR == 0) return fail(FT_ERR_SHAPE, "empty reduction");
+  if (!a || !as || !at || !wq || !ws || !wt || !out) return fail(FT_ERR_NULL, "every operand is required");
+  if (!aligned16(a) || !aligned16(as) || !aligned16(wq) || !aligned16(ws) || !aligned16(out) ||
+      ((uintptr_t)at & 3u) || ((uintptr_t)wt & 3u))
+    return fail(FT_ERR_ALIGN, "codes, scales and out must be 16-byte aligned, tensor scales 4-byte aligned");
+  if ((int64_t)M * KR / 2 >= ((int64_t)1 << 31) || (int64_t)M * NO >= ((int64_t)1 << 31))
+    return fail(FT_ERR_SHAPE, "operands too large for this path");
+  const int N = (int)(bwd ? KR : NO), K = (int)(bwd ? NO : KR);
+  return hip_status(ft::launch_gemm_nvfp4(bwd, a, as, at, wq, ws, wt, (int)M, N, K, out, stream), "gemm nvfp4");
+}
+
+ft_status ft_linear_fwd_nvfp4(const uint8_t* xq, const uint8_t* xs, const float* xt, int64_t M, int64_t K,
+                              const uint8_t* wq, const uint8_t* ws, const float* wt, int64_t N, float* y,
+                              hipStream_t stream) {
+  g_last_error[0] = 0;
+  return nvfp4_gemm(false, xq, xs, xt, M, K, wq, ws, wt, N, y, stream);
+}
+
+ft_status ft_linear_bwd_input_nvfp4(const uint8_t* gq, const uint8_t* gs, const float* gt, int64_t M, int64_t N,
+                                    const uint8_t* wq, const uint8_t* ws, const float* wt, int64_t K, float* dx,
+                                    hipStream_t stream) {
+  g_last_error[0] = 0;
+  return nvfp4_gemm(true, gq, gs, gt, M, N, wq, ws, wt, K, dx, stream);
+}
+
 }  // extern "C"

@@ -69,4 +69,12 @@ hipError_t launch_lora_grads(const uint16_t* x, int M, int K, const uint16_t* dy
 constexpr size_t kLoraScratchBytes = (size_t)32 << 20;
 hipError_t lora_grads_scratch(float** ptr);
 
+// NVFP4 emulation: quantization (1x16 or 16x16 blocks, E4M3 scales, the fp32
+// tensor scale left in *tensor_scale) and the dequantizing bf16-MFMA GEMM
+// (fp32 output, both tensor scales applied).
+hipError_t launch_quant_nvfp4(const uint16_t* src, int rows, int cols, int block_rows, uint8_t* codes,
+                              uint8_t* scales, float* tensor_scale, hipStream_t st);
+hipError_t launch_gemm_nvfp4(bool bwd, const uint8_t* a, const uint8_t* as, const float* at, const uint8_t* wq,
+                             const uint8_t* ws, const float* wt, int M, int N, int K, float* out, hipStream_t st);
+
 }  // namespace ft

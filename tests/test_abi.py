@@ -236,3 +236,21 @@ def test_quantize_mode_validation():
     assert call(M(0, 0, 0, 0, 0), rows=-1) == _lib.FT_ERR_SHAPE
     assert f(ALIGNED, 64, 64, 1, ALIGNED, MISALIGNED, NULL, 0, 0, NULL, NULL, 0, None, NULL) == _lib.FT_ERR_ALIGN
     assert f(NULL, 0, 64, 1, NULL, NULL, NULL, 0, 0, NULL, NULL, 0, None, NULL) == _lib.FT_OK
+
+
+def test_nvfp4_validation():
+    L = _lib.load()
+    q = L.ft_quantize_nvfp4
+    assert q(ALIGNED, 16, 24, 1, ALIGNED, ALIGNED2, ALIGNED, NULL) == _lib.FT_ERR_SHAPE        # cols % 16
+    assert q(ALIGNED, 24, 32, 16, ALIGNED, ALIGNED2, ALIGNED, NULL) == _lib.FT_ERR_SHAPE       # rows % 16 for tiles
+    assert q(ALIGNED, 16, 32, 8, ALIGNED, ALIGNED2, ALIGNED, NULL) == _lib.FT_ERR_UNSUPPORTED
+    assert q(ALIGNED, 16, 32, 1, ALIGNED, ALIGNED2, NULL, NULL) == _lib.FT_ERR_NULL
+    assert q(ALIGNED, 16, 32, 1, ALIGNED, MISALIGNED, ALIGNED, NULL) == _lib.FT_ERR_ALIGN
+    assert q(NULL, 0, 32, 1, NULL, NULL, NULL, NULL) == _lib.FT_OK
+    f = L.ft_linear_fwd_nvfp4
+    assert f(ALIGNED, ALIGNED, ALIGNED, 8, 40, ALIGNED, ALIGNED, ALIGNED, 32, ALIGNED2, NULL) == _lib.FT_ERR_SHAPE
+    assert f(ALIGNED, ALIGNED, NULL, 8, 32, ALIGNED, ALIGNED, ALIGNED, 32, ALIGNED2, NULL) == _lib.FT_ERR_NULL
+    assert f(ALIGNED, ALIGNED, ALIGNED, 8, 0, ALIGNED, ALIGNED, ALIGNED, 32, ALIGNED2, NULL) == _lib.FT_ERR_SHAPE
+    b = L.ft_linear_bwd_input_nvfp4
+    assert b(ALIGNED, ALIGNED, ALIGNED, 8, 32, ALIGNED, ALIGNED, ALIGNED, 48, MISALIGNED, NULL) == _lib.FT_ERR_ALIGN
+    assert b(NULL, NULL, NULL, 0, 32, NULL, NULL, NULL, 48, NULL, NULL) == _lib.FT_OK
