@@ -56,6 +56,8 @@ def parse():
                     help="flux_qkv / flux_mlp: time the fused step against an unfused one, print one JSON line, exit")
     ap.add_argument("--numerics", action="store_true",
                     help="time the quantizer's numerics variants at the QKV shapes, print one JSON line, exit")
+    ap.add_argument("--dit", action="store_true",
+                    help="time one synthetic FLUX DiT training step, W4A4G4 against BF16 LoRA; print one JSON line")
     ap.add_argument("--stability", action="store_true",
                     help="run the synthetic gradient-norm stability probe, print one JSON line, exit")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -642,6 +644,49 @@ def stability_probe(torch, L, dev, seed, steps=150, M=4096, K=1024, N=1024, r=16
             "variants": summary}
 
 
+def dit_step_timing(torch, dev, seed, steps, warmup, cfg=None):
+    """One synthetic FLUX.1-dev DiT training step (19 double + 38 single
+    blocks at 4096 image + 512 text tokens; forward, loss, backward, AdamW on
+    the LoRA factors) with the W4A4G4 layers, and the same step with BF16
+    LoRA linears (the paper's comparison, Sec. 4 "Efficiency Results")."""
+    from paper_2607_05711_amd import dit
+    cfg = cfg or dit.FLUX_DEV
+    out = {}
+    for kind in ("fp4", "bf16"):
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats(dev)
+        model = dit.DiT(cfg, kind, seed, dev)
+        trainer = dit.Trainer(model)
+        batch = dit.synthetic_batch(cfg, seed + 1, dev)
+        wbytes = sum(t.numel() * t.element_size() for m in model.modules()
+                     for t in ([m.wq, m.ws] if isinstance(m, dit.FourTuneLinear) else
+                               [m.W] if isinstance(m, dit.Bf16LoraLinear) else []))
+        for _ in range(warmup):
+            trainer.step(*batch)
+        torch.cuda.synchronize()
+        a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a_.record()
+        for _ in range(steps):
+            loss = trainer.step(*batch)
+        b_.record()
+        torch.cuda.synchronize()
+        out[kind] = {"ms_per_step": round(a_.elapsed_time(b_) / steps, 2), "loss": round(float(loss), 5),
+                     "peak_memory_gb": round(torch.cuda.max_memory_allocated(dev) / 1e9, 2),
+                     "linear_weight_gb": round(wbytes / 1e9, 2)}
+        del model, trainer, batch
+        print("dit %s: %.2f ms/step" % (kind, out[kind]["ms_per_step"]), file=sys.stderr, flush=True)
+    return {"metric": "synthetic FLUX.1-dev DiT training step time, W4A4G4 vs BF16 LoRA", "unit": "ms",
+            "w4a4g4": out["fp4"], "bf16_lora": out["bf16"],
+            "speedup_vs_bf16_lora": round(out["bf16"]["ms_per_step"] / out["fp4"]["ms_per_step"], 3),
+            "config": {"double_blocks": cfg.double_blocks, "single_blocks": cfg.single_blocks,
+                       "img_tokens": cfg.img_tokens, "txt_tokens": cfg.txt_tokens, "hidden": cfg.hidden,
+                       "heads": cfg.heads, "mlp": cfg.mlp, "lora_rank": cfg.lora_rank,
+                       "stabilizer_rank": cfg.stab_rank},
+            "step": "forward, MSE loss, backward, AdamW on every LoRA factor; attention, norms, modulation "
+                    "and RoPE as torch operations (fused attention kernels only)",
+            "steps": steps, "warmup": warmup, "data": "synthetic, random weights"}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -662,6 +707,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.numerics:
         print(json.dumps(numerics_timing(torch, _lib, dev, args.seed, args.steps, args.warmup)), flush=True)
+        return
+    if args.dit:
+        print(json.dumps(dit_step_timing(torch, dev, args.seed, args.steps, args.warmup)), flush=True)
         return
     if args.stability:
         print(json.dumps(stability_probe(torch, _lib, dev, args.seed)), flush=True)
@@ -709,6 +757,12 @@ def main():
                     others[name][k] = o[k]
             torch.cuda.empty_cache()
             print("measured %s: %.3f ms/step" % (name, o["ms_per_step"]), file=sys.stderr, flush=True)
+        # the synthetic DiT training step, W4A4G4 against BF16 LoRA; a failure here is reported, not hidden
+        try:
+            others["flux_dit"] = dit_step_timing(torch, dev, args.seed, 3, 2)
+        except Exception as e:   # noqa: BLE001
+            others["flux_dit"] = {"error": "%s: %s" % (type(e).__name__, e)}
+        torch.cuda.empty_cache()
         out["other_workloads"] = others
     if not args.no_cpu_baseline:
         if d is None:
