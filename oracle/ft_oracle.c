@@ -606,21 +606,28 @@ int fto_lora_grads(const uint16_t *x, int64_t M, int64_t K, const uint16_t *g, i
 
 /* ------------------------------------------------------------------ GELU */
 
-/* GELU, tanh form: 0.5 z (1 + tanh(c (z + 0.044715 z^3))), c = sqrt(2/pi). */
+/* GELU, tanh form: 0.5 z (1 + tanh(u)), u = c (z + 0.044715 z^3), c = sqrt(2/pi).
+ * Evaluated as z / (1 + exp(-2u)): 0.5 (1 + tanh u) = 1 / (1 + exp(-2u)) is the
+ * same function, and this form does not lose the small values of 1 + tanh u
+ * for very negative u to cancellation. */
 double fto_gelu(double z)
 {
     const double c = sqrt(2.0 / M_PI);
-    return 0.5 * z * (1.0 + tanh(c * (z + 0.044715 * z * z * z)));
+    const double u = c * (z + 0.044715 * z * z * z);
+    return z / (1.0 + exp(-2.0 * u));
 }
 
-/* d/dz of fto_gelu. */
+/* d/dz of fto_gelu: 0.5 (1 + tanh u) + 0.5 z (1 - tanh^2 u) u', written with
+ * s = 0.5 (1 + tanh u) = 1 / (1 + exp(-2u)) and 1 - s = 1 / (1 + exp(2u))
+ * (each without cancellation), 1 - tanh^2 u = 4 s (1 - s). */
 double fto_gelu_grad(double z)
 {
     const double c = sqrt(2.0 / M_PI);
-    double u = c * (z + 0.044715 * z * z * z);
-    double th = tanh(u);
-    double du = c * (1.0 + 3.0 * 0.044715 * z * z);
-    return 0.5 * (1.0 + th) + 0.5 * z * (1.0 - th * th) * du;
+    const double u = c * (z + 0.044715 * z * z * z);
+    const double s = 1.0 / (1.0 + exp(-2.0 * u));
+    const double t = 1.0 / (1.0 + exp(2.0 * u));
+    const double du = c * (1.0 + 3.0 * 0.044715 * z * z);
+    return s + 2.0 * z * s * t * du;
 }
 
 /* Elementwise GELU / GELU' over n doubles (convenience for tests). */

@@ -204,12 +204,47 @@ def test_gelu_closed_forms():
     assert gl[0] == 0.0 and gd[0] == 0.5
     assert gl[1] == 50.0 and gd[1] == 1.0
     assert gl[2] == 0.0 and abs(gd[2]) < 1e-300
-    # 0.5 (1 + tanh u) = sigmoid(2u)
+    # the tanh form as printed, where 1 + tanh u does not cancel
     c = np.sqrt(2 / np.pi)
     u = c * (z + 0.044715 * z ** 3)
-    with np.errstate(over="ignore"):
-        alt = z / (1.0 + np.exp(-2.0 * u))
-    assert np.allclose(gl, alt, rtol=1e-14, atol=1e-300)
+    keep = z > -3
+    assert np.allclose(gl[keep], (0.5 * z * (1.0 + np.tanh(u)))[keep], rtol=1e-14, atol=1e-300)
+
+
+def _gelu_decimal(z, derivative=False):
+    """GELU (tanh form) and its derivative from the definition, in 60-digit
+    decimal arithmetic, with e = e^{2u}: tanh u = (e - 1) / (e + 1), so
+    1 + tanh u = 2e / (e + 1) and 1 - tanh^2 u = 4e / (e + 1)^2 exactly (kept in
+    these forms: 60 digits would not hold 1 + tanh u for u below -70)."""
+    from decimal import Decimal, getcontext
+    getcontext().prec = 60
+    zd = Decimal(float(z))
+    c = (Decimal(2) / Decimal("3.14159265358979323846264338327950288419716939937510582097494")).sqrt()
+    u = c * (zd + Decimal("0.044715") * zd ** 3)
+    e = (2 * u).exp()
+    one_plus_th = 2 * e / (e + 1)
+    if not derivative:
+        return float(Decimal("0.5") * zd * one_plus_th)
+    du = c * (1 + 3 * Decimal("0.044715") * zd ** 2)
+    one_minus_th2 = 4 * e / (e + 1) ** 2
+    return float(Decimal("0.5") * one_plus_th + Decimal("0.5") * zd * one_minus_th2 * du)
+
+
+def test_gelu_against_definition_in_high_precision():
+    # the definition evaluated in 60 digits, across the range the bf16 tables
+    # cover: both signs, tiny to large |z|, including the far negative tail
+    # where 1 + tanh u is tiny
+    zs = [s * m * 2.0 ** e for s in (1, -1) for e in range(-12, 5) for m in (1.0, 1.3, 1.7)]
+    zs += [-6.0, -8.0, -10.0, -11.0, -13.5, -15.9]
+    # The bound follows the conditioning: u itself carries one fp64 rounding,
+    # which exp(-2u) turns into a relative error of about 2|u| ulp.
+    c = np.sqrt(2 / np.pi)
+    for z in zs:
+        g, d = ref.gelu(np.array([z]))[0], ref.gelu(np.array([z]), derivative=True)[0]
+        gx, dx = _gelu_decimal(z), _gelu_decimal(z, True)
+        tol = 2.0 ** -52 * (8 + 4 * abs(c * (z + 0.044715 * z ** 3)))
+        assert abs(g - gx) <= tol * abs(gx), (z, g, gx)
+        assert abs(d - dx) <= tol * abs(dx) + 1e-300, (z, d, dx)
 
 
 def test_gelu_derivative_finite_difference():
