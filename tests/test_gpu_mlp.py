@@ -288,6 +288,33 @@ def test_mlp_pair_flux_shape_sampled():
     assert np.all(np.abs(host(P2)[rows] - pr_or) <= proj_bound(F, 48, pa_or) + moved * (1 + 1e-6))
 
 
+@pytest.mark.parametrize("M", [200, 256])
+def test_fused_epilogues_are_deterministic(M):
+    """Repeated calls on the same inputs give the same bits: z, h, codes,
+    scales and P2 of FC1; dz, codes, scales and Qp1 of FC2 (several column
+    tiles, a partial row tile at M = 200)."""
+    rng = np.random.default_rng(M)
+    K, F, R = 256, 1024, 32
+    X, W1, W2 = rand_bf16(rng, (M, K), 1.0), rand_bf16(rng, (F, K), 0.05), rand_bf16(rng, (K, F), 0.05)
+    D1, U1 = rand_bf16(rng, (K, R), 0.05), rand_bf16(rng, (R, F), 0.05)
+    D2, U2 = rand_bf16(rng, (F, R), 0.05), rand_bf16(rng, (R, K), 0.05)
+    dY = rand_bf16(rng, (M, K), 0.01)
+    w1q, w1s, _ = _lib.ft_quantize_blockwise(dev_bf16(W1), block_rows=32)
+    w2q, w2s, _ = _lib.ft_quantize_blockwise(dev_bf16(W2), block_rows=32)
+    xq, xs, P1 = _lib.ft_quantize_blockwise(dev_bf16(X), proj=dev_bf16(D1))
+    gq, gs, Qp2 = _lib.ft_quantize_blockwise(dev_bf16(dY), proj=dev_bf16(U2), proj_layout=_lib.FT_PROJ_R_BY_COLS)
+    runs = []
+    for _ in range(4):
+        fwd = _lib.ft_linear_fwd_gelu(xq, xs, w1q, w1s, K, P1, dev_bf16(U1), None, D2=dev_bf16(D2))
+        bwd = _lib.ft_linear_bwd_input_dgelu(gq, gs, w2q, w2s, F, fwd[0], Qp2, dev_bf16(D2), U1=dev_bf16(U1))
+        runs.append([t.clone() for t in list(fwd) + list(bwd)])
+    torch.cuda.synchronize()
+    names = ["z", "h", "hq", "hs", "P2", "dz", "dzq", "dzs", "Qp1"]
+    for k, name in enumerate(names):
+        for r in runs[1:]:
+            assert torch.equal(runs[0][k], r[k]), name + " differs between identical calls"
+
+
 def test_mlp_empty_token_axis():
     """M = 0 through both fused epilogues: the calls succeed and every output
     with a token axis is empty."""
