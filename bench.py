@@ -644,6 +644,65 @@ def stability_probe(torch, L, dev, seed, steps=150, M=4096, K=1024, N=1024, r=16
             "variants": summary}
 
 
+LIBRARY_GEMM_TEXT = ("hipBLASLt's MXFP4 GEMM through torch._scaled_mm (E2M1 operands, one E8M0 scale per 1x32 "
+                     "block of each operand, bf16 output) against this library's FP4 GEMM without the low-rank "
+                     "branch and the bias, on the same random codes and scales (the weight's 32x32 tile scales "
+                     "repeated per row for the library); for the backward-input shape the library gets a "
+                     "pre-transposed weight (random codes of that shape), while this library reads the forward's "
+                     "codes transposed. Back-to-back calls, warm. Context only: neither is the layer step.")
+
+
+def library_gemm(torch, _lib, dev, seed, steps=20, warmup=5):
+    """Plain MXFP4 GEMM times (us) of the vendor library and of this library at
+    the FLUX shapes: forward Q(X) Q(W)^T and backward-input Q(dY) Q(W)."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+
+    def codes(r, c):
+        return torch.randint(0, 256, (r, c // 2), dtype=torch.uint8, device=dev, generator=g)
+
+    def scales(r, c):
+        return torch.randint(120, 131, (r, c), dtype=torch.uint8, device=dev, generator=g)
+
+    def time_us(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps * 1e3
+
+    e2m1, e8m0 = torch.float4_e2m1fn_x2, torch.float8_e8m0fnu
+    out = {"what": LIBRARY_GEMM_TEXT}
+    for name, M, K, N in (("qkv", 4608, 3072, 9216), ("mlp_fc1", 4608, 3072, 12288)):
+        wq, ws = codes(N, K), scales(N // 32, K // 32)
+        ws_rows = ws.repeat_interleave(32, dim=0).contiguous()
+        # forward: [M, K] x [N, K]^T
+        xq, xs = codes(M, K), scales(M, K // 32)
+        lib_f = time_us(lambda: torch._scaled_mm(xq.view(e2m1), wq.view(e2m1).t(), xs.view(e8m0), ws_rows.view(e8m0),
+                                                 out_dtype=torch.bfloat16))
+        ours_f = time_us(lambda: _lib.ft_linear_fwd(xq, xs, wq, ws, K))
+        # backward-input: [M, N] x [N, K]; the library takes W^T [K, N] with scales along N
+        gq, gs = codes(M, N), scales(M, N // 32)
+        wtq = codes(K, N)
+        wts = ws.t().repeat_interleave(32, dim=0).contiguous()
+        lib_b = time_us(lambda: torch._scaled_mm(gq.view(e2m1), wtq.view(e2m1).t(), gs.view(e8m0), wts.view(e8m0),
+                                                 out_dtype=torch.bfloat16))
+        ours_b = time_us(lambda: _lib.ft_linear_bwd_input(gq, gs, wq, ws, K))
+        fl = 2.0 * M * N * K
+        out[name] = {"shape": [M, K, N],
+                     "fwd_us": {"library": round(lib_f, 2), "ours": round(ours_f, 2)},
+                     "bwd_us": {"library": round(lib_b, 2), "ours": round(ours_b, 2)},
+                     "fwd_tflops": {"library": round(fl / lib_f / 1e6, 1), "ours": round(fl / ours_f / 1e6, 1)},
+                     "bwd_tflops": {"library": round(fl / lib_b / 1e6, 1), "ours": round(fl / ours_b / 1e6, 1)}}
+        torch.cuda.empty_cache()
+    return out
+
+
 def dit_step_timing(torch, dev, seed, steps, warmup, cfg=None):
     """One synthetic FLUX.1-dev DiT training step (19 double + 38 single
     blocks at 4096 image + 512 text tokens; forward, loss, backward, AdamW on
@@ -764,6 +823,10 @@ def main():
             others["flux_dit"] = {"error": "%s: %s" % (type(e).__name__, e)}
         torch.cuda.empty_cache()
         out["other_workloads"] = others
+        try:
+            out["library_gemm"] = library_gemm(torch, _lib, dev, args.seed)
+        except Exception as e:   # noqa: BLE001
+            out["library_gemm"] = {"error": "%s: %s" % (type(e).__name__, e)}
     if not args.no_cpu_baseline:
         if d is None:
             shape = gen.SHAPES["flux_qkv"]
