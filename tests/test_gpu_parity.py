@@ -53,6 +53,7 @@ def proj_bound(cols, pabs):
 def check_gemm(out32, out16, refv, S, what):
     err = np.abs(out32.astype(np.float64) - refv)
     worst = (err / np.maximum(S, 1e-300)).max()
+    print("%s: max err/S = %.3g" % (what, worst), flush=True)
     assert np.all(err <= 1e-5 * S), "%s: max err/S = %.3g" % (what, worst)
     assert np.array_equal(out16, bf16_rne_of_f32(out32)), "%s: bf16 output is not RNE of the fp32 result" % what
     err16 = np.abs(f64(out16) - refv)
@@ -356,6 +357,34 @@ def test_gemm_pipelined_shapes(M, K, N, R):
     check_gemm(host(y32), host(y16), yr, S, "forward")
     dxr, Sdx = ref.linear_bwd_input(gq, gs, wq, ws, K, f(Qp), D)
     check_gemm(host(dx32), host(dx16), dxr, Sdx, "backward-input")
+
+
+@pytest.mark.parametrize("K", [12288, 15360])
+def test_long_reduction_rounds_once_per_mfma_step(K):
+    """One fp32 accumulator per output over the whole reduction, rounded once
+    per 64-element MFMA step.  Adversarial codes: the first step contributes
+    1, every later one a single product of 2^-24 = half an ulp of the running
+    sum, which round-half-to-even drops.  The error may then reach
+    (K/64 - 1) 2^-24 S, above 1e-5 S from K = 10752 on, but never more than
+    K/64 roundings of at most 2^-24 of the running |sum| allow."""
+    M, N = 40, 64
+    steps = K // 64
+    xq = np.zeros((M, K // 2), np.uint8)
+    wq = np.zeros((N, K // 2), np.uint8)
+    xq[:, ::32] = 0x02            # element 64 j = 1.0 (E2M1 code 2, low nibble)
+    wq[:, ::32] = 0x02
+    xs = np.full((M, K // 32), 127, np.uint8)
+    ws = np.full((N // 32, K // 32), 127, np.uint8)
+    xs[:, 2::2] = 115             # blocks holding k = 64 j, j >= 1: 2^-12
+    ws[:, 2::2] = 115             # so every later product is 2^-12 * 2^-12 = 2^-24
+    y32 = host(_lib.ft_linear_fwd(dev_u8(xq), dev_u8(xs), dev_u8(wq), dev_u8(ws), K, out_dtype=torch.float32))
+    torch.cuda.synchronize()
+    yr, S = ref.linear_fwd(xq, xs, wq, ws, K, None, None)
+    assert np.all(yr == 1.0 + (steps - 1) * 2.0 ** -24)
+    err = np.abs(y32.astype(np.float64) - yr)
+    print("K = %d: max err / S = %.3g (1e-5 bar; bound %d x 2^-24 = %.3g)" % (K, (err / S).max(), steps,
+                                                                            steps * 2.0 ** -24), flush=True)
+    assert np.all(err <= steps * 2.0 ** -24 * S)
 
 
 def test_layer_flux_qkv_full_size_sampled():
