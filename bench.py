@@ -23,7 +23,10 @@ import argparse
 import hashlib
 import json
 import os
+import signal
+import subprocess
 import sys
+import tempfile
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -746,6 +749,83 @@ def dit_step_timing(torch, dev, seed, steps, warmup, cfg=None):
             "steps": steps, "warmup": warmup, "data": "synthetic, random weights"}
 
 
+def start_clock_sampler():
+    """rocm-smi's clocks and power, sampled every few tenths of a second by a shell loop
+    started before this process touches the GPU (so no child process is
+    started from a process holding a GPU context).  Lines: '<unix time> <json>'.
+    Returns (process, path) or (None, None) when rocm-smi is not there."""
+    if not any(os.access(os.path.join(d, "rocm-smi"), os.X_OK) for d in os.environ.get("PATH", "").split(os.pathsep)):
+        return None, None
+    fd, path = tempfile.mkstemp(prefix="ft_clock_", suffix=".txt")
+    # it polls only while <path>.go exists, so the timed steps run without it
+    script = ("while true; do if [ -e '%s.go' ]; then t=$(date +%%s.%%N); "
+              "o=$(timeout 10 rocm-smi --showclocks --showpower --json 2>/dev/null | tr -d '\\n'); "
+              "echo \"$t $o\"; sleep 0.2; else sleep 0.05; fi; done") % path
+    proc = subprocess.Popen(["bash", "-c", script], stdout=fd, stderr=subprocess.DEVNULL, start_new_session=True)
+    os.close(fd)
+    return proc, path
+
+
+def stop_clock_sampler(proc, path):
+    if proc is None:
+        return
+    try:
+        os.killpg(proc.pid, signal.SIGTERM)
+    except ProcessLookupError:
+        pass
+    proc.wait(timeout=10)
+    for p in (path, path + ".go"):
+        try:
+            os.unlink(p)
+        except OSError:
+            pass
+
+
+def clock_under_load(torch, fn, path, seconds=2.0):
+    """Run fn back to back for `seconds` and return the rocm-smi samples taken
+    meanwhile: graphics clock (MHz) and package power (W)."""
+    if path is None:
+        return {"error": "rocm-smi not found"}
+    fn()
+    torch.cuda.synchronize()
+    open(path + ".go", "w").close()
+    t0 = time.time()
+    calls = 0
+    while time.time() - t0 < seconds:
+        for _ in range(10):
+            fn()
+        calls += 10
+        torch.cuda.synchronize()
+    t1 = time.time()
+    time.sleep(1.0)   # let a sample taken in the window finish writing
+    os.unlink(path + ".go")
+    sclk, mclk, power = [], [], []
+    with open(path) as f:
+        for line in f:
+            parts = line.strip().split(" ", 1)
+            if len(parts) != 2:
+                continue
+            try:
+                t, d = float(parts[0]), json.loads(parts[1]).get("card0", {})
+            except ValueError:
+                continue
+            if not t0 + 0.2 <= t <= t1 - 0.5:   # the sample's rocm-smi call ran inside the window
+                continue
+            for k, v in d.items():
+                if k.startswith("sclk clock speed"):
+                    sclk.append(float(v.strip("()").lower().replace("mhz", "")))
+                elif k.startswith("mclk clock speed"):
+                    mclk.append(float(v.strip("()").lower().replace("mhz", "")))
+                elif "power" in k.lower() and "max" not in k.lower():
+                    try:
+                        power.append(float(str(v).split()[0]))
+                    except ValueError:
+                        pass
+    return {"what": "rocm-smi samples while the forward GEMM of the QKV step runs back to back",
+            "seconds": round(t1 - t0, 2), "calls": calls, "sclk_mhz": sclk, "mclk_mhz": mclk,
+            "power_w": power if power else "not reported by rocm-smi here"}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -758,6 +838,15 @@ def main():
         copy_calibration(args.copy_calibration)
         return
 
+    default_line = not (args.numerics or args.dit or args.stability or args.ablation)
+    sampler, sample_path = start_clock_sampler() if default_line and args.workload == "flux_qkv" else (None, None)
+    try:
+        run(args, sample_path)
+    finally:
+        stop_clock_sampler(sampler, sample_path)
+
+
+def run(args, sample_path):
     import torch
     from paper_2607_05711_amd import _lib, gen
 
@@ -802,6 +891,17 @@ def main():
         "config": rec["config"],
     }
     out.update({k: v for k, v in rec.items() if k not in ("tflops", "ms_per_step", "config")})
+    if sample_path is not None:
+        try:
+            K = d["X"].shape[1]
+            xq, xs, P = _lib.ft_quantize_blockwise(d["X"], proj=d["D"])
+            wq, ws, _ = _lib.ft_quantize_blockwise(d["W"], block_rows=32)
+            ybuf = torch.empty((d["X"].shape[0], d["W"].shape[0]), dtype=torch.bfloat16, device=dev)
+            out["gpu_clock"] = clock_under_load(
+                torch, lambda: _lib.ft_linear_fwd(xq, xs, wq, ws, K, P, d["U"], d["bias"], y=ybuf), sample_path)
+            del xq, xs, P, wq, ws, ybuf
+        except Exception as e:   # noqa: BLE001
+            out["gpu_clock"] = {"error": "%s: %s" % (type(e).__name__, e)}
     if args.workload == "flux_qkv" and not args.no_other_workloads:
         # the other FLUX configurations, each as its own whole step (fewer steps)
         others = {}
