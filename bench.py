@@ -897,8 +897,14 @@ def run(args, sample_path):
             xq, xs, P = _lib.ft_quantize_blockwise(d["X"], proj=d["D"])
             wq, ws, _ = _lib.ft_quantize_blockwise(d["W"], block_rows=32)
             ybuf = torch.empty((d["X"].shape[0], d["W"].shape[0]), dtype=torch.bfloat16, device=dev)
-            out["gpu_clock"] = clock_under_load(
+            gc = clock_under_load(
                 torch, lambda: _lib.ft_linear_fwd(xq, xs, wq, ws, K, P, d["U"], d["bias"], y=ybuf), sample_path)
+            rf = out.get("roofline") or {}
+            if gc.get("sclk_mhz") and rf.get("achieved") and rf.get("peak"):
+                mhz = sorted(gc["sclk_mhz"])[len(gc["sclk_mhz"]) // 2]
+                # the dense MXFP4 peak scales with the clock: 16384 FLOP per clock per CU
+                gc["gemm_fwd_frac_at_median_sclk"] = round(rf["achieved"] / (rf["peak"] * mhz / 2400.0), 4)
+            out["gpu_clock"] = gc
             del xq, xs, P, wq, ws, ybuf
         except Exception as e:   # noqa: BLE001
             out["gpu_clock"] = {"error": "%s: %s" % (type(e).__name__, e)}
