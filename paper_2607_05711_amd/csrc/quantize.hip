@@ -52,7 +52,7 @@ __device__ __forceinline__ uint32_t quad_max(uint32_t m) {
   return m;
 }
 
-// One 64-column step of a wave's 32 rows (4 groups of 8 rows): block
+// One 64-column step of a wave's 8*NQ rows (NQ groups of 8 rows): block
 // scales and codes, the scale bytes staged in the wave's LDS rows, and (XT)
 // the step's bf16 values in the wave's projection tile.  EDGE: rows past
 // the end and blocks past the chunk are zeroed and not stored.
@@ -60,13 +60,13 @@ __device__ __forceinline__ uint32_t quad_max(uint32_t m) {
 // index (row * cols + column) of this lane's first element in group q = 0 and
 // rstep8 = 8 * cols (the next group's rows); one Philox call draws the
 // uniforms of the lane's 8 elements.
-template <bool EDGE, bool XT, int QM = 0, class Store>
+template <bool EDGE, bool XT, int QM = 0, int NQ = 4, class Store>
 __device__ __forceinline__ void quant_step(const v4i (&x)[4], int rw0, int rows, bool col_ok, int lr, int lc,
                                            int lane, const Store& store, int st, FT_LDS uint8_t* sc,
                                            int sc_row, FT_LDS uint16_t* xt, const SrKey& key = SrKey{},
                                            uint64_t idx0 = 0, uint64_t rstep8 = 0) {
 #pragma unroll
-  for (int q = 0; q < 4; q++) {
+  for (int q = 0; q < NQ; q++) {
     const int row = rw0 + 8 * q + lr;
     const bool ok = !EDGE || (col_ok && row < rows);
     uint32_t w[4];
@@ -270,16 +270,18 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
 }
 
 // ---------------------------------------------------------------- full rows
-// Projection [cols, R] only.  Workgroup = WAVES waves over 32 whole rows;
-// wave w takes the 64-column steps w, w + WAVES, ...  A step is handled as in
+// Projection [cols, R] only.  Workgroup = WAVES waves over ROWS = 8*NQ whole
+// rows (32, or 24 when that fills more CUs); wave w takes the 64-column
+// steps w, w + WAVES, ...  A step is handled as in
 // k_quant_rows: row-contiguous loads (every 8 lanes read one 128-byte line),
 // block scales and codes from lane quads, the bf16 values through a private
 // LDS tile into the MFMA layout.  The step's 64 projection rows come with it,
 // also as whole 128-byte lines, into a second private tile that is read back
 // transposed.  The waves' partial projections are added in LDS in wave
 // order: nothing partial leaves the workgroup and no reduction kernel
-// follows.  The price is one read of the projection matrix (from L2) per 32
-// rows, on fewer workgroups than the chunked kernel has.
+// follows.  The price is one read of the projection matrix (from L2) per
+// workgroup, on fewer workgroups than the chunked kernel has.  With 24 rows
+// the MFMA tile's last 8 rows are zeros and their results are dropped.
 constexpr int QF_MAX_BLOCKS = 128;   // scale bytes per row staged in LDS: cols <= 4096
 
 template <int RT, int WAVES>
@@ -293,7 +295,7 @@ struct QuantFrLds {
   static constexpr int BYTES = WORK + 32 * QF_MAX_BLOCKS;
 };
 
-template <int RT, int WAVES, int QM>
+template <int RT, int WAVES, int QM, int NQ>
 __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __restrict__ src, int rows, int cols,
                                                               uint8_t* __restrict__ codes,
                                                               uint8_t* __restrict__ scales,
@@ -307,7 +309,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int row0 = blockIdx.x * 32;
+  constexpr int ROWS = 8 * NQ;
+  const int row0 = blockIdx.x * ROWS;
   const int lr = lane >> 3, lc = (lane & 7) * 8;     // row within an 8-row group, column within a step
   const int nsteps = (cols + 63) >> 6;
   const int nmine = wave < nsteps ? (nsteps - 1 - wave) / WAVES + 1 : 0;
@@ -322,9 +325,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(src, (uint32_t)((size_t)rows * cols * 2));
   const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes, (uint32_t)((size_t)rows * cols / 2));
   const __amdgpu_buffer_rsrc_t rp = make_rsrc(proj, (uint32_t)((size_t)R * cols * 2));
-  uint32_t xoff[4], coff[4], poff[NP];
+  uint32_t xoff[NQ], coff[NQ], poff[NP];
 #pragma unroll
-  for (int q = 0; q < 4; q++) {
+  for (int q = 0; q < NQ; q++) {
     const int r = row0 + 8 * q + lr;
     xoff[q] = r < rows ? (uint32_t)(r * cols + lc) * 2u : kOobOffset;
     coff[q] = r < rows ? (uint32_t)(r * (cols >> 1) + (lc >> 1)) : kOobOffset;
@@ -340,14 +343,14 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __
 
   auto step_of = [&](int k) { return wave + k * WAVES; };
 
-  struct Ops { v4i x[4]; v4i p[NP]; };
+  struct Ops { v4i x[4]; v4i p[NP]; };   // x[q] for q < NQ
   // Loads of local step k.  On the last step of a row whose length is an odd
   // multiple of 32, the upper lanes read past the row; quant_step zeroes those
   // values (the projection rows there lie past the buffer).
   auto issue = [&](int k, Ops& o) {
     const int c = 64 * step_of(k);
 #pragma unroll
-    for (int q = 0; q < 4; q++) o.x[q] = __builtin_amdgcn_raw_buffer_load_b128(rx, xoff[q], 2 * c, 0);
+    for (int q = 0; q < NQ; q++) o.x[q] = __builtin_amdgcn_raw_buffer_load_b128(rx, xoff[q], 2 * c, 0);
 #pragma unroll
     for (int q = 0; q < NP; q++)
       o.p[q] = __builtin_amdgcn_raw_buffer_load_b128(rp, poff[q], 2 * c * R, 0);
@@ -357,18 +360,23 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __
 #pragma unroll
   for (int t = 0; t < RT; t++) acc[t] = v16f{};
   const int r32 = lane & 31, h = lane >> 5, g16 = lane >> 4, t16 = lane & 15;
+  if constexpr (ROWS < 32) {
+    // rows ROWS..31 of the wave's bf16 tile stay zero: the steps write rows < ROWS only
+    for (int e = lane; e < (32 - ROWS) * (QR_XSTRIDE / 8); e += 64)
+      *(FT_LDS v4i*)(xt + ROWS * QR_XSTRIDE + 8 * e) = v4i{0, 0, 0, 0};
+  }
 
   auto consume = [&](int k, Ops& o) {
     const int st = step_of(k), c = 64 * st;
     const int blk = 2 * st + (lane >> 2 & 1);
     const bool col_ok = blk < nbc;
     const uint64_t idx0 = (uint64_t)(row0 + lr) * cols + c + lc;
-    if (row0 + 32 > rows || c + 64 > cols)
-      quant_step<true, true, QM>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt, key, idx0,
-                                 8ull * cols);
+    if (row0 + ROWS > rows || c + 64 > cols)
+      quant_step<true, true, QM, NQ>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt, key,
+                                     idx0, 8ull * cols);
     else
-      quant_step<false, true, QM>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt, key, idx0,
-                                  8ull * cols);
+      quant_step<false, true, QM, NQ>(o.x, row0, rows, col_ok, lr, lc, lane, store, st, sc, QF_MAX_BLOCKS, xt, key,
+                                      idx0, 8ull * cols);
     // the step's projection rows
 #pragma unroll
     for (int q = 0; q < NP; q++) {
@@ -420,13 +428,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __
 #pragma unroll
     for (int w = 0; w < WAVES; w++) sum += red[w * NOUT + o];
     const int t = o >> 10, v = (o >> 6) & 15, ln = o & 63;
-    const int r = row0 + 8 * (v >> 2) + 4 * (ln >> 5) + (v & 3), j = t * 32 + (ln & 31);
-    if (r < rows && j < R) proj_out[(size_t)r * R + j] = sum;
+    const int rl = 8 * (v >> 2) + 4 * (ln >> 5) + (v & 3), r = row0 + rl, j = t * 32 + (ln & 31);
+    if (rl < ROWS && r < rows && j < R) proj_out[(size_t)r * R + j] = sum;
   }
   // scale bytes of the workgroup's rows
   const int nw = (nbc + 3) >> 2;
   const bool al = (nbc & 3) == 0;
-  for (int d = tid; d < 32 * nw; d += NT) {
+  for (int d = tid; d < ROWS * nw; d += NT) {
     const int rr = d / nw, dw = d % nw, r = row0 + rr;
     if (r >= rows) continue;
     uint8_t* dst = scales + (size_t)r * nbc + 4 * dw;
@@ -506,8 +514,12 @@ static int quant_chunk_cols(int rows, int cols, int R, int layout) {
 // larger projection matrix (4608 x 15360: 94 us against 80).  For proj
 // [R, cols] at 4608 x 9216 the chunked kernel is faster (33 against 36 us):
 // the step work of 4608 rows on 144 workgroups outweighs the partial sums.
+// Rows per whole-row workgroup: 24 when that still makes one round (more CUs
+// busy than with 32), else 32.
+static int quant_fr_rows(int rows) { return (rows + 23) / 24 <= 256 ? 24 : 32; }
+
 static bool quant_full_rows(int rows, int cols, int R, int layout) {
-  const int wg = (rows + 31) / 32;
+  const int wg = (rows + quant_fr_rows(rows) - 1) / quant_fr_rows(rows);
   return layout == 0 && R > 0 && R <= 64 && cols <= 32 * QF_MAX_BLOCKS && wg >= 64 && wg <= 256;
 }
 
@@ -539,9 +551,13 @@ static hipError_t launch_quant_rows_qm(const uint16_t* src, int rows, int cols, 
     return launch_rows_t<1, 0, 4, 384, QM>(src, rows, cols, codes, scales, nullptr, 0, nullptr, nullptr, key, st);
   const int rt = (R + 31) / 32;
   if (quant_full_rows(rows, cols, R, layout)) {
-    const unsigned grid = (unsigned)((rows + 31) / 32);
-    if (rt == 1) k_quant_rows_fr<1, 8, QM><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, key);
-    else k_quant_rows_fr<2, 8, QM><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, key);
+    const int fr = quant_fr_rows(rows);
+    const unsigned grid = (unsigned)((rows + fr - 1) / fr);
+#define FT_FR(RT_, NQ_) \
+  k_quant_rows_fr<RT_, 8, QM, NQ_><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, key)
+    if (fr == 24) { if (rt == 1) FT_FR(1, 3); else FT_FR(2, 3); }
+    else { if (rt == 1) FT_FR(1, 4); else FT_FR(2, 4); }
+#undef FT_FR
     return hipGetLastError();
   }
 #define FT_ROWS(RT_, MODE_, CW_) \

@@ -103,11 +103,12 @@ def test_quantize_tiles_bitexact(rows, cols):
                                                 # rows longer than 4096: column chunks, ragged last chunk
                                                 (2304, 10976, 64, 0),
                                                 # [cols, R] with whole rows per workgroup (64..256 workgroups
-                                                # of 32 rows, rows up to 4096): ragged rows, a last half step,
-                                                # fewer steps than waves, projections narrower than their
-                                                # 32-column tiles
+                                                # of 24 rows, or of 32 when 24 would need more than 256; rows
+                                                # up to 4096): ragged rows, a last half step, fewer steps than
+                                                # waves, projections narrower than their 32-column tiles
                                                 (2304, 4064, 64, 0), (2200, 1056, 16, 0), (2100, 160, 64, 0),
-                                                (8192, 800, 48, 0), (2080, 96, 32, 0),
+                                                (8192, 800, 48, 0), (2080, 96, 32, 0), (1601, 512, 64, 0),
+                                                (7001, 288, 64, 0),
                                                 # [R, cols] at the same row counts (column chunks)
                                                 (2065, 4160, 64, 1), (3000, 2080, 32, 1), (2080, 640, 48, 1)])
 def test_quantize_fused_projection(rows, cols, R, layout):
