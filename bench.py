@@ -63,6 +63,8 @@ def parse():
                     help="time one synthetic FLUX DiT training step, W4A4G4 against BF16 LoRA; print one JSON line")
     ap.add_argument("--stability", action="store_true",
                     help="run the synthetic gradient-norm stability probe, print one JSON line, exit")
+    ap.add_argument("--no-clock-sample", action="store_true",
+                    help="skip the rocm-smi clock sample (2 s of back-to-back forward GEMMs) of the default line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (scales HBM counters), then exit")
     return ap.parse_args()
@@ -839,7 +841,8 @@ def main():
         return
 
     default_line = not (args.numerics or args.dit or args.stability or args.ablation)
-    sampler, sample_path = start_clock_sampler() if default_line and args.workload == "flux_qkv" else (None, None)
+    sample = default_line and args.workload == "flux_qkv" and not args.no_clock_sample
+    sampler, sample_path = start_clock_sampler() if sample else (None, None)
     try:
         run(args, sample_path)
     finally:
