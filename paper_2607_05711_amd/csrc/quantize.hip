@@ -283,6 +283,11 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
 // workgroup, on fewer workgroups than the chunked kernel has.  With 24 rows
 // the MFMA tile's last 8 rows are zeros and their results are dropped.
 constexpr int QF_MAX_BLOCKS = 128;   // scale bytes per row staged in LDS: cols <= 4096
+// Waves per whole-row workgroup: 10 (at most 5 of a 48-step row each) where
+// the kernel fits 168 VGPRs without spilling, else 8 (stochastic rounding,
+// 32-row workgroups).
+template <int QM, int NQ>
+constexpr int fr_waves() { return ((QM & QM_SR) != 0 || NQ == 4) ? 8 : 10; }
 
 template <int RT, int WAVES>
 struct QuantFrLds {
@@ -305,7 +310,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows_fr(const uint16_t* __
   __shared__ __attribute__((aligned(16))) uint8_t lds[L::BYTES];
   constexpr int NT = 64 * WAVES;
   constexpr int NP = 4 * RT;        // 16-byte projection loads per lane and step
-  constexpr int NB = 3;             // step buffers: two steps in flight ahead of the one consumed
+  constexpr int NB = WAVES > 8 ? 2 : 3;   // step buffers: NB - 1 steps in flight ahead of the one consumed
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -554,7 +559,8 @@ static hipError_t launch_quant_rows_qm(const uint16_t* src, int rows, int cols, 
     const int fr = quant_fr_rows(rows);
     const unsigned grid = (unsigned)((rows + fr - 1) / fr);
 #define FT_FR(RT_, NQ_) \
-  k_quant_rows_fr<RT_, 8, QM, NQ_><<<grid, 512, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out, key)
+  k_quant_rows_fr<RT_, fr_waves<QM, NQ_>(), QM, NQ_><<<grid, 64 * fr_waves<QM, NQ_>(), 0, st>>>(src, rows, cols, codes, \
+                                                                                            scales, proj, R, proj_out, key)
     if (fr == 24) { if (rt == 1) FT_FR(1, 3); else FT_FR(2, 3); }
     else { if (rt == 1) FT_FR(1, 4); else FT_FR(2, 4); }
 #undef FT_FR
