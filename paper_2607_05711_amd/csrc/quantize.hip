@@ -512,15 +512,15 @@ static int quant_chunk_cols(int rows, int cols, int R, int layout) {
   return (R + 31) / 32 <= 2 ? 768 : 384;
 }
 
-// Whole rows per workgroup (no partial sums) for proj [cols, R] when 32-row
-// workgroups make between 64 and one round of 256, rows are at most 4096
-// long and the projection is at most 64 wide (4608 x 3072: 16.5 us against
-// 17.8 with the chunks' reduction).  Longer rows make each workgroup read a
-// larger projection matrix (4608 x 15360: 94 us against 80).  For proj
-// [R, cols] at 4608 x 9216 the chunked kernel is faster (33 against 36 us):
-// the step work of 4608 rows on 144 workgroups outweighs the partial sums.
-// Rows per whole-row workgroup: 24 when that still makes one round (more CUs
-// busy than with 32), else 32.
+// Whole rows per workgroup (no partial sums) for proj [cols, R] when the
+// whole-row workgroups make between 64 and one round of 256, rows are at
+// most 4096 long and the projection is at most 64 wide (4608 x 3072: 12.8 to
+// 13.5 us, against 13.1 plus a 4.7 us reduction for the chunks).  Longer rows
+// make each workgroup read a larger projection matrix (4608 x 15360: 94 us
+// against 80).  For proj [R, cols] at 4608 x 9216 the chunked kernel is
+// faster (33 against 36 us): the step work of 4608 rows outweighs the
+// partial sums.  Rows per whole-row workgroup: 24 when that still makes one
+// round (more CUs busy than with 32), else 32.
 static int quant_fr_rows(int rows) { return (rows + 23) / 24 <= 256 ? 24 : 32; }
 
 static bool quant_full_rows(int rows, int cols, int R, int layout) {
