@@ -508,6 +508,15 @@ __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict_
 // while the chunk fits LDS.
 static int quant_chunk_cols(int rows, int cols, int R, int layout) {
   if (R == 0) return 384;
+  const int rt = (R + 31) / 32;
+  // rows longer than 4096: the widest chunk whose projection slice fits LDS,
+  // so fewer partial sums (4608 x 15360, R = 64: 61-62 us at 384 columns,
+  // 58 at 512, 49-51 at 640; 18432 x 15360, R = 96: 300 at 384, 280 at 512),
+  // as long as it still makes a full round of workgroups
+  if (layout == 0 && cols > 4096) {
+    const int wide = rt <= 2 ? 640 : rt == 3 ? 512 : 384;
+    if ((size_t)((rows + 255) / 256) * ((cols + wide - 1) / wide) >= 256) return wide;
+  }
   if (layout == 0) return (size_t)((rows + 255) / 256) * ((cols + 383) / 384) < 256 ? 256 : 384;
   return (R + 31) / 32 <= 2 ? 768 : 384;
 }
@@ -569,7 +578,10 @@ static hipError_t launch_quant_rows_qm(const uint16_t* src, int rows, int cols, 
 #define FT_ROWS(RT_, MODE_, CW_) \
   launch_rows_t<RT_, MODE_, 8, CW_, QM>(src, rows, cols, codes, scales, proj, R, proj_out, ws, key, st)
   if (layout == 0) {
-    if (quant_chunk_cols(rows, cols, R, layout) == 256) {
+    const int cw = quant_chunk_cols(rows, cols, R, layout);
+    if (cw == 640) return rt == 1 ? FT_ROWS(1, 1, 640) : FT_ROWS(2, 1, 640);
+    if (cw == 512) return FT_ROWS(3, 1, 512);
+    if (cw == 256) {
       switch (rt) {
         case 1: return FT_ROWS(1, 1, 256);
         case 2: return FT_ROWS(2, 1, 256);

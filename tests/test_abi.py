@@ -84,10 +84,14 @@ def test_quantize_validation():
     need = _lib.ft_quantize_workspace_size(512, 3072, 1, 64, 0)
     assert need == 12 * 512 * 64 * 4       # 256-column chunks: 384 would leave fewer workgroups than CUs
     assert _lib.ft_quantize_workspace_size(8224, 3072, 1, 64, 0) == 8 * 8224 * 64 * 4     # 384 otherwise
-    assert _lib.ft_quantize_workspace_size(18432, 15360, 1, 96, 0) == 40 * 18432 * 96 * 4
+    # rows longer than 4096: the widest chunk that fits LDS (512 for R = 96, 640 for R <= 64) while it
+    # still makes a full round of workgroups, else as above
+    assert _lib.ft_quantize_workspace_size(18432, 15360, 1, 96, 0) == 30 * 18432 * 96 * 4
+    assert _lib.ft_quantize_workspace_size(4608, 15360, 1, 64, 0) == 24 * 4608 * 64 * 4
+    assert _lib.ft_quantize_workspace_size(2304, 10976, 1, 64, 0) == 29 * 2304 * 64 * 4     # 640 would make 162
     assert _lib.ft_quantize_workspace_size(512, 9216, 1, 64, 1) == 12 * 512 * 64 * 4     # 768 for [R, cols]
     assert _lib.ft_quantize_workspace_size(512, 256, 1, 64, 0) == 0                      # one chunk: none
-    # whole rows per workgroup for [cols, R] (64..256 workgroups of 32 rows, R <= 64): no partial sums
+    # whole rows per workgroup for [cols, R] (64..256 workgroups of 24 or 32 rows, R <= 64): no partial sums
     assert _lib.ft_quantize_workspace_size(4608, 3072, 1, 64, 0) == 0
     assert _lib.ft_quantize_workspace_size(4608, 15360, 1, 64, 0) > 0                    # rows > 4096: chunks
     assert _lib.ft_quantize_workspace_size(4608, 9216, 1, 64, 1) == 12 * 4608 * 64 * 4   # [R, cols]: chunks

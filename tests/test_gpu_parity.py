@@ -102,6 +102,10 @@ def test_quantize_tiles_bitexact(rows, cols):
                                                 (8224, 3072, 64, 0),
                                                 # rows longer than 4096: column chunks, ragged last chunk
                                                 (2304, 10976, 64, 0),
+                                                # ... in 640-column chunks (R <= 64) or 512 (R = 96) when
+                                                # those still make 256 workgroups; ragged rows, last chunks
+                                                # of one step, a step and a half, half a step
+                                                (8200, 6464, 64, 0), (8200, 5216, 32, 0), (8200, 5152, 96, 0),
                                                 # [cols, R] with whole rows per workgroup (64..256 workgroups
                                                 # of 24 rows, or of 32 when 24 would need more than 256; rows
                                                 # up to 4096): ragged rows, a last half step, fewer steps than
