@@ -518,7 +518,9 @@ static int quant_chunk_cols(int rows, int cols, int R, int layout) {
     if ((size_t)((rows + 255) / 256) * ((cols + wide - 1) / wide) >= 256) return wide;
   }
   if (layout == 0) return (size_t)((rows + 255) / 256) * ((cols + 383) / 384) < 256 ? 256 : 384;
-  return (R + 31) / 32 <= 2 ? 768 : 384;
+  // [R, cols]: the widest chunk whose projection slice fits LDS (18432 x 21504
+  // with R = 96: 416-437 us at 384 columns, 385-400 at 512)
+  return rt <= 2 ? 768 : rt == 3 ? 512 : 384;
 }
 
 // Whole rows per workgroup (no partial sums) for proj [cols, R] when the
@@ -599,7 +601,7 @@ static hipError_t launch_quant_rows_qm(const uint16_t* src, int rows, int cols, 
   switch (rt) {
     case 1: return FT_ROWS(1, 2, 768);
     case 2: return FT_ROWS(2, 2, 768);
-    case 3: return FT_ROWS(3, 2, 384);
+    case 3: return FT_ROWS(3, 2, 512);
     default: return FT_ROWS(4, 2, 384);
   }
 #undef FT_ROWS

@@ -113,8 +113,10 @@ def test_quantize_tiles_bitexact(rows, cols):
                                                 (2304, 4064, 64, 0), (2200, 1056, 16, 0), (2100, 160, 64, 0),
                                                 (8192, 800, 48, 0), (2080, 96, 32, 0), (1601, 512, 64, 0),
                                                 (7001, 288, 64, 0),
-                                                # [R, cols] at the same row counts (column chunks)
-                                                (2065, 4160, 64, 1), (3000, 2080, 32, 1), (2080, 640, 48, 1)])
+                                                # [R, cols] at the same row counts (column chunks; 512 columns
+                                                # for R = 96)
+                                                (2065, 4160, 64, 1), (3000, 2080, 32, 1), (2080, 640, 48, 1),
+                                                (1000, 5152, 96, 1)])
 def test_quantize_fused_projection(rows, cols, R, layout):
     rng = np.random.default_rng(rows + cols + R)
     bits = random_rows("outliers", rows, cols, seed=rows)
