@@ -509,11 +509,12 @@ __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict_
 static int quant_chunk_cols(int rows, int cols, int R, int layout) {
   if (R == 0) return 384;
   const int rt = (R + 31) / 32;
-  // rows longer than 4096: the widest chunk whose projection slice fits LDS,
-  // so fewer partial sums (4608 x 15360, R = 64: 61-62 us at 384 columns,
-  // 58 at 512, 49-51 at 640; 18432 x 15360, R = 96: 300 at 384, 280 at 512),
-  // as long as it still makes a full round of workgroups
-  if (layout == 0 && cols > 4096) {
+  // the widest chunk whose projection slice fits LDS, so fewer partial sums,
+  // as long as it still makes a full round of workgroups (4608 x 15360,
+  // R = 64: 61-62 us at 384 columns, 58 at 512, 49-51 at 640; 18432 x 15360,
+  // R = 96: 300 at 384, 280 at 512; 18432 x 3072: 58-61 -> 50-53 us at
+  // R = 96, 49-50 -> 42-43 at R = 64)
+  if (layout == 0) {
     const int wide = rt <= 2 ? 640 : rt == 3 ? 512 : 384;
     if ((size_t)((rows + 255) / 256) * ((cols + wide - 1) / wide) >= 256) return wide;
   }

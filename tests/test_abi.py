@@ -84,11 +84,12 @@ def test_quantize_validation():
     need = _lib.ft_quantize_workspace_size(512, 3072, 1, 64, 0)
     assert need == 12 * 512 * 64 * 4       # 256-column chunks: 384 would leave fewer workgroups than CUs
     assert _lib.ft_quantize_workspace_size(8224, 3072, 1, 64, 0) == 8 * 8224 * 64 * 4     # 384 otherwise
-    # rows longer than 4096: the widest chunk that fits LDS (512 for R = 96, 640 for R <= 64) while it
-    # still makes a full round of workgroups, else as above
+    # the widest chunk that fits LDS (512 for R = 96, 640 for R <= 64) while it still makes a full
+    # round of workgroups, else as above
     assert _lib.ft_quantize_workspace_size(18432, 15360, 1, 96, 0) == 30 * 18432 * 96 * 4
     assert _lib.ft_quantize_workspace_size(4608, 15360, 1, 64, 0) == 24 * 4608 * 64 * 4
     assert _lib.ft_quantize_workspace_size(2304, 10976, 1, 64, 0) == 29 * 2304 * 64 * 4     # 640 would make 162
+    assert _lib.ft_quantize_workspace_size(18432, 3072, 1, 96, 0) == 6 * 18432 * 96 * 4
     assert _lib.ft_quantize_workspace_size(512, 9216, 1, 64, 1) == 12 * 512 * 64 * 4     # 768 for [R, cols]
     assert _lib.ft_quantize_workspace_size(512, 9216, 1, 96, 1) == 18 * 512 * 96 * 4     # 512 at R = 96
     assert _lib.ft_quantize_workspace_size(512, 256, 1, 64, 0) == 0                      # one chunk: none

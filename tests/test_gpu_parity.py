@@ -106,6 +106,8 @@ def test_quantize_tiles_bitexact(rows, cols):
                                                 # those still make 256 workgroups; ragged rows, last chunks
                                                 # of one step, a step and a half, half a step
                                                 (8200, 6464, 64, 0), (8200, 5216, 32, 0), (8200, 5152, 96, 0),
+                                                # ... and for rows of at most 4096 when those fill a round
+                                                (13200, 3136, 64, 0), (11000, 3104, 96, 0),
                                                 # [cols, R] with whole rows per workgroup (64..256 workgroups
                                                 # of 24 rows, or of 32 when 24 would need more than 256; rows
                                                 # up to 4096): ragged rows, a last half step, fewer steps than
