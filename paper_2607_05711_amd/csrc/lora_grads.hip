@@ -222,8 +222,11 @@ __global__ __launch_bounds__(256) void k_lora_grads(LoraJob jb0, LoraJob jb1, in
   else lora_tile<RTJ, false>(job, lds, cg * LG_WC, mbeg, mend, ld, r, part, accumulate);
 }
 
-// Token chunking: enough workgroups for one round.  Every ring takes more
-// than half of LDS (96 KB or more), so a CU holds one workgroup.
+// Token chunking: the fewest rounds of workgroups that keep at least 90 % of
+// the CUs busy (one round at the QKV and MLP shapes; two for the single-
+// stream shapes, where one round of 96 column groups left a quarter of the
+// CUs idle: 18432 x (3072 + 21504) 268-287 -> 249-275 us).  Every ring takes
+// more than half of LDS (96 KB or more), so a CU holds one workgroup.
 static void lg_geometry(int rows, int K, int N, int r, int& nmch, int& mchunk) {
   const int rtj = (r + 31) / 32;
   const int slot_bytes = LG_VBYTES + LG_BM * rtj * 128, ns = rtj == 1 ? 3 : 2;
@@ -231,6 +234,13 @@ static void lg_geometry(int rows, int K, int N, int r, int& nmch, int& mchunk) {
   const int ncg = (N + LG_WC - 1) / LG_WC + (K + LG_WC - 1) / LG_WC;
   const int mblocks = (rows + LG_BM - 1) / LG_BM;
   nmch = std::max(1, std::min(mblocks, slots / ncg));
+  for (int k = 1; k <= 4; k++) {
+    const int c = std::min(mblocks, k * slots / ncg);
+    if (c >= 1 && (double)ncg * c >= 0.9 * k * slots) {
+      nmch = c;
+      break;
+    }
+  }
   mchunk = ((mblocks + nmch - 1) / nmch) * LG_BM;
   nmch = (rows + mchunk - 1) / mchunk;
 }
