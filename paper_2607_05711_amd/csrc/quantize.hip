@@ -520,7 +520,11 @@ static int quant_chunk_cols(int rows, int cols, int R, int layout) {
   }
   if (layout == 0) return (size_t)((rows + 255) / 256) * ((cols + 383) / 384) < 256 ? 256 : 384;
   // [R, cols]: the widest chunk whose projection slice fits LDS (18432 x 21504
-  // with R = 96: 416-437 us at 384 columns, 385-400 at 512)
+  // with R = 96: 416-437 us at 384 columns, 385-400 at 512; 4608 x 9216 with
+  // R = 64: 28.8 us at 768, 36-37 at 256 or 384), except that 256-column
+  // chunks fill the chip when 768-column ones would make fewer than 128
+  // workgroups (4608 x 3072: 20.4 -> 16.1 us; 512 x 3072: 17.3 -> 13.8)
+  if (rt <= 2 && (size_t)((rows + 255) / 256) * ((cols + 767) / 768) < 128) return 256;
   return rt <= 2 ? 768 : rt == 3 ? 512 : 384;
 }
 
@@ -599,6 +603,7 @@ static hipError_t launch_quant_rows_qm(const uint16_t* src, int rows, int cols, 
       default: return FT_ROWS(4, 1, 384);
     }
   }
+  if (quant_chunk_cols(rows, cols, R, layout) == 256) return rt == 1 ? FT_ROWS(1, 2, 256) : FT_ROWS(2, 2, 256);
   switch (rt) {
     case 1: return FT_ROWS(1, 2, 768);
     case 2: return FT_ROWS(2, 2, 768);

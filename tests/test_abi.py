@@ -90,7 +90,8 @@ def test_quantize_validation():
     assert _lib.ft_quantize_workspace_size(4608, 15360, 1, 64, 0) == 24 * 4608 * 64 * 4
     assert _lib.ft_quantize_workspace_size(2304, 10976, 1, 64, 0) == 29 * 2304 * 64 * 4     # 640 would make 162
     assert _lib.ft_quantize_workspace_size(18432, 3072, 1, 96, 0) == 6 * 18432 * 96 * 4
-    assert _lib.ft_quantize_workspace_size(512, 9216, 1, 64, 1) == 12 * 512 * 64 * 4     # 768 for [R, cols]
+    assert _lib.ft_quantize_workspace_size(4608, 9216, 1, 64, 1) == 12 * 4608 * 64 * 4   # 768 for [R, cols]
+    assert _lib.ft_quantize_workspace_size(512, 9216, 1, 64, 1) == 36 * 512 * 64 * 4     # 256: 768 makes 24
     assert _lib.ft_quantize_workspace_size(512, 9216, 1, 96, 1) == 18 * 512 * 96 * 4     # 512 at R = 96
     assert _lib.ft_quantize_workspace_size(512, 256, 1, 64, 0) == 0                      # one chunk: none
     # whole rows per workgroup for [cols, R] (64..256 workgroups of 24 or 32 rows, R <= 64): no partial sums

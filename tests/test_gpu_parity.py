@@ -115,10 +115,11 @@ def test_quantize_tiles_bitexact(rows, cols):
                                                 (2304, 4064, 64, 0), (2200, 1056, 16, 0), (2100, 160, 64, 0),
                                                 (8192, 800, 48, 0), (2080, 96, 32, 0), (1601, 512, 64, 0),
                                                 (7001, 288, 64, 0),
-                                                # [R, cols] at the same row counts (column chunks; 512 columns
-                                                # for R = 96)
+                                                # [R, cols] at the same row counts (column chunks: 256 columns
+                                                # where 768 would make fewer than 128 workgroups, 512 for
+                                                # R = 96) and with 768-column chunks and a ragged last one
                                                 (2065, 4160, 64, 1), (3000, 2080, 32, 1), (2080, 640, 48, 1),
-                                                (1000, 5152, 96, 1)])
+                                                (1000, 5152, 96, 1), (4352, 6400, 64, 1)])
 def test_quantize_fused_projection(rows, cols, R, layout):
     rng = np.random.default_rng(rows + cols + R)
     bits = random_rows("outliers", rows, cols, seed=rows)
