@@ -987,9 +987,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     uint8_t* sbuf = lds + 4 * STG + PSLICE + wave * 512;
     uint8_t* qbuf = lds + 4 * STG + PSLICE + 4 * 512 + wave * (128 * 64);
     static_assert(4 * STG + PSLICE + 4 * 512 + (QLDS ? 4 * 128 * 64 : 0) <= NSLOT * SLOT, "epilogue LDS");
-    // After the passes, the projection partials of the two waves that share
-    // rows are added in [2 row halves][128 rows][64] fp32 at the start of LDS.
-    static_assert(2 * 128 * 64 * 4 <= 4 * STG + PSLICE, "combine area below the code buffers");
+    // After the passes and the code flush, the projection partials of the two
+    // waves that share rows are added through four [128 rows][64] fp32
+    // regions at the start of LDS.
     const int R2 = ep.R2;
     const int tn = nt;
     // The projection slice: rows n0..n0+255 of D2 [NO, R2], or columns
@@ -1143,48 +1143,17 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         }
       }
     }
-    if (R2 > 0) {
-      // 4) the two waves with the same rows (wn = 0, 1) add their partials,
-      //    all passes at once, in LDS the passes no longer use; each then
-      //    stores half of the summed rows as 16-byte segments
-      __syncthreads();
-      float* cb = (float*)lds + wm * (128 * 64);
-      if (wn == 1) {
-#pragma unroll
-        for (int i = 0; i < 4; i++)
-#pragma unroll
-          for (int t = 0; t < 2; t++)
-#pragma unroll
-            for (int v = 0; v < 16; v++)
-              cb[(32 * i + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * t + r32] = acc[i][t][v];
-      }
-      __syncthreads();
-      if (wn == 0) {
-#pragma unroll
-        for (int i = 0; i < 4; i++)
-#pragma unroll
-          for (int t = 0; t < 2; t++)
-#pragma unroll
-            for (int v = 0; v < 16; v++)
-              cb[(32 * i + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * t + r32] += acc[i][t][v];
-      }
-      __syncthreads();
-      float* dst = tiles_n > 1 ? ep.parts + (size_t)tn * M * R2 : ep.parts;
-#pragma unroll
-      for (int q = 0; q < 16; q++) {
-        const int rr = 64 * wn + 4 * q + (lane >> 4), j = 4 * (lane & 15);
-        const int gr = orow0 + rr;
-        if (j < R2 && gr < M) *(float4*)(dst + (size_t)gr * R2 + j) = *(const float4*)(cb + rr * 64 + j);
-      }
-    }
-    // E2M1 codes (EPI_GELU): 16 bytes (32 columns) of a row per lane
+    // E2M1 codes (EPI_GELU): 16 bytes (32 columns) of a row per lane, all
+    // reads first, then branch-free stores (outside rows and columns dropped)
     if constexpr (QLDS) {
+      v4i cq[8];
+#pragma unroll
+      for (int q = 0; q < 8; q++) cq[q] = *(const v4i*)(qbuf + (16 * q + (lane >> 2)) * 64 + 16 * (lane & 3));
 #pragma unroll
       for (int q = 0; q < 8; q++) {
-        const int rr = 16 * q + (lane >> 2), c = lane & 3;
-        const int gr = orow0 + rr;
-        if (gr < M && ocol0 + 32 * c < NO)
-          *(v4i*)(ep.q + (size_t)gr * (NO / 2) + (ocol0 / 2) + 16 * c) = *(const v4i*)(qbuf + rr * 64 + 16 * c);
+        const int gr = orow0 + 16 * q + (lane >> 2), c = lane & 3;
+        __builtin_amdgcn_raw_buffer_store_b128(
+            cq[q], r_q, (gr < M && ocol0 + 32 * c < NO) ? (uint32_t)gr * (NO / 2) + (ocol0 / 2) + 16 * c : kOobOffset, 0, 0);
       }
     }
     // E8M0 codes: each lane writes rows lane and lane + 64 of the wave's 128,
@@ -1203,6 +1172,43 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
           for (int b = 0; b < 4; b++)
             if (ocol0 + 32 * b < NO) d[b] = (uint8_t)(v >> (8 * b));
         }
+      }
+    }
+    if (R2 > 0) {
+      // 4) the two waves with the same rows (wn = 0, 1) add their partials,
+      //    all passes at once: each wave stores its own in a 32 KB region
+      //    (the code buffers are flushed, so all of LDS is free), and after
+      //    one barrier each wave adds the two partials of half of its rows
+      //    and stores the sums as 16-byte segments
+      static_assert(4 * 128 * 64 * 4 <= NSLOT * SLOT, "combine regions");
+      __syncthreads();   // every wave is done with the passes' LDS and its code buffers
+      float* mine = (float*)lds + (2 * wn + wm) * (128 * 64);
+#pragma unroll
+      for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int t = 0; t < 2; t++)
+#pragma unroll
+          for (int v = 0; v < 16; v++)
+            mine[(32 * i + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * t + r32] = acc[i][t][v];
+      __syncthreads();
+      // all reads first, then branch-free stores (rows past M and columns
+      // past R2 go to an offset past the buffer, which drops them)
+      const float* c0 = (const float*)lds + wm * (128 * 64);          // the wn = 0 partial
+      const float* c1 = (const float*)lds + (2 + wm) * (128 * 64);    // the wn = 1 partial
+      float* dst = tiles_n > 1 ? ep.parts + (size_t)tn * M * R2 : ep.parts;
+      const __amdgpu_buffer_rsrc_t rdst = make_rsrc(dst, (uint32_t)M * R2 * 4);
+      const int j = 4 * (lane & 15);
+      v4f sum[16];
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int rr = 64 * wn + 4 * q + (lane >> 4);
+        sum[q] = *(const v4f*)(c1 + rr * 64 + j) + *(const v4f*)(c0 + rr * 64 + j);
+      }
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int gr = orow0 + 64 * wn + 4 * q + (lane >> 4);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, sum[q]), rdst,
+                                               (j < R2 && gr < M) ? ((uint32_t)gr * R2 + j) * 4 : kOobOffset, 0, 0);
       }
     }
   }
