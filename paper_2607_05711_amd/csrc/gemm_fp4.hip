@@ -1123,24 +1123,31 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       __builtin_amdgcn_s_waitcnt(0xc07f);
       // 3) projection of the pass's 32 rows over this wave's 128 columns, into
       //    the pass's first two accumulator tiles (read out in step 1)
+      //    Both 32-column slice tiles are always used (the slice holds zeros
+      //    past R2), and the fragments of k-step ks + 1 are read while the
+      //    MFMAs of k-step ks run.
       acc[i][0] = v16f{};
       acc[i][1] = v16f{};
-#pragma unroll
-      for (int ks = 0; ks < 8; ks++) {
-        const v8bf a = __builtin_bit_cast(v8bf, *(const v4i*)(stg + r32 * SROW + (16 * ks + 8 * h) * 2));
+      auto frag = [&](int ks, v8bf& a, v8bf (&b)[2]) {
+        a = __builtin_bit_cast(v8bf, *(const v4i*)(stg + r32 * SROW + (16 * ks + 8 * h) * 2));
         const int kloc = wn * 128 + 16 * ks + 8 * h;      // column within the workgroup's 256
 #pragma unroll
         for (int t = 0; t < 2; t++) {
-          if (t >= rt2) break;
-          v8bf b;
           if constexpr (G) {
             const uint16_t* base = ps + (kloc + jj) * PS1 + 32 * t + 16 * (g16 & 1) + 4 * qq;
-            b = make_v8bf(lds_read_tr16((const FT_LDS void*)base), lds_read_tr16((const FT_LDS void*)(base + 4 * PS1)));
+            b[t] = make_v8bf(lds_read_tr16((const FT_LDS void*)base), lds_read_tr16((const FT_LDS void*)(base + 4 * PS1)));
           } else {
-            b = __builtin_bit_cast(v8bf, *(const v4i*)(ps + (32 * t + r32) * PS2 + kloc));
+            b[t] = __builtin_bit_cast(v8bf, *(const v4i*)(ps + (32 * t + r32) * PS2 + kloc));
           }
-          acc[i][t] = mfma_bf16_32x32x16(a, b, acc[i][t]);
         }
+      };
+      v8bf fa[2], fb[2][2];
+      frag(0, fa[0], fb[0]);
+#pragma unroll
+      for (int ks = 0; ks < 8; ks++) {
+        if (ks + 1 < 8) frag(ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
+#pragma unroll
+        for (int t = 0; t < 2; t++) acc[i][t] = mfma_bf16_32x32x16(fa[ks & 1], fb[ks & 1][t], acc[i][t]);
       }
     }
     // E2M1 codes (EPI_GELU): 16 bytes (32 columns) of a row per lane, all
