@@ -233,6 +233,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 // An offset no buffer here reaches: a load from it returns zeros.
 constexpr uint32_t kOobOffset = 0x80000000u;
 
+// Cache policy of buffer stores whose data no kernel reads soon (GEMM outputs,
+// the MLP epilogues' activations and codes): non-temporal, so they stream to
+// HBM without displacing operand lines from L2.
+constexpr int kStoreNT = 2;
+
 // Buffer resource words for the asm loads below (same layout as make_rsrc).
 __device__ __forceinline__ v4i rsrc_words(const void* base, uint32_t bytes) {
   const uint64_t a = (uint64_t)base;

@@ -955,7 +955,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       for (int it = 0; it < 8; it++) {
         const int gr = orow0 + 32 * i + 4 * it + (lane >> 4), gc = ocol0 + 8 * (lane & 15);
         const uint32_t off = (gr < M && gc < NO) ? ((uint32_t)gr * NO + gc) * 2 : kOobOffset;
-        __builtin_amdgcn_raw_buffer_store_b128(seg[it], ro, off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(seg[it], ro, off, 0, kStoreNT);
       }
     }
   } else {
@@ -1093,7 +1093,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         uint32_t w[4];
         if constexpr (G) {
           const v4i zb = *(const v4i*)(srow + seg * 16);
-          __builtin_amdgcn_raw_buffer_store_b128(zb, r_z, off2, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(zb, r_z, off2, 0, kStoreNT);
 #pragma unroll
           for (int e = 0; e < 4; e++) {
             const v2f hv = {gelu_tanh(bf16_to_f32((uint32_t)zb[e] & 0xFFFFu)), gelu_tanh(bf16_to_f32((uint32_t)zb[e] >> 16))};
@@ -1111,7 +1111,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
           }
         }
         const v4i wv = {(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-        __builtin_amdgcn_raw_buffer_store_b128(wv, r_y, off2, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(wv, r_y, off2, 0, kStoreNT);
         *(v4i*)(srow + seg * 16) = wv;   // bf16 result in place (for the projection)
         uint32_t sc;
         const uint32_t codes = quad_quantize8(w, sc);
@@ -1160,7 +1160,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
       for (int q = 0; q < 8; q++) {
         const int gr = orow0 + 16 * q + (lane >> 2), c = lane & 3;
         __builtin_amdgcn_raw_buffer_store_b128(
-            cq[q], r_q, (gr < M && ocol0 + 32 * c < NO) ? (uint32_t)gr * (NO / 2) + (ocol0 / 2) + 16 * c : kOobOffset, 0, 0);
+            cq[q], r_q, (gr < M && ocol0 + 32 * c < NO) ? (uint32_t)gr * (NO / 2) + (ocol0 / 2) + 16 * c : kOobOffset, 0, kStoreNT);
       }
     }
     // E8M0 codes: each lane writes rows lane and lane + 64 of the wave's 128,
