@@ -143,27 +143,25 @@ __device__ __forceinline__ float e8m0_to_f32(uint32_t code) {
 }
 
 // tanh-approximated GELU, 0.5 z (1 + tanh(u)) with u = c0 (z + c1 z^3), and
-// its derivative, in fp32.  u has the sign of z; with
-// e = exp(-2|u|) = 2^(|z| (a + b z^2)), a = -2 c0 log2(e), b = a c1 (e <= 1,
-// so it never overflows) and r = 1 / (1 + e):
-//   0.5 (1 + tanh u) = r for z >= 0, e r for z < 0;   1 - tanh(u)^2 = 4 e r^2;
-//   GELU(z)  = z r or z e r (no cancellation for very negative z),
-//   GELU'(z) = 0.5 (1 + tanh u) + z e r^2 (2 c0 + 6 c0 c1 z^2).
+// its derivative, in fp32.  With e = exp(-2u) = 2^(z (a + b z^2)),
+// a = -2 c0 log2(e), b = a c1, and r = 1 / (1 + e) = 0.5 (1 + tanh u):
+//   GELU(z)  = z r,
+//   GELU'(z) = r + z r (1 - r) (2 c0 + 6 c0 c1 z^2)      (1 - tanh(u)^2 = 4 r (1 - r)).
+// For very negative z, e overflows to +inf and r is 0: GELU(z) = -0 and
+// GELU'(z) = 0, where the exact values are below 2^-120 in magnitude.
 constexpr float kGeluA = -2.302208198e+00f;   // -2 sqrt(2/pi) log2(e)
 constexpr float kGeluB = -1.029432396e-01f;   // kGeluA * 0.044715
 constexpr float kGeluG1 = 1.595769122e+00f;  // 2 sqrt(2/pi)
 constexpr float kGeluG3 = 2.140644488e-01f;  // 6 sqrt(2/pi) 0.044715
 __device__ __forceinline__ float gelu_tanh(float z) {
-  const float e = __builtin_amdgcn_exp2f(fabsf(z) * fmaf(kGeluB, z * z, kGeluA));
-  const float r = __builtin_amdgcn_rcpf(1.0f + e);   // hardware reciprocal (1 ulp)
-  return (z >= 0.0f ? z : z * e) * r;
+  const float e = __builtin_amdgcn_exp2f(z * fmaf(kGeluB, z * z, kGeluA));
+  return z * __builtin_amdgcn_rcpf(1.0f + e);   // hardware reciprocal (1 ulp)
 }
 __device__ __forceinline__ float gelu_tanh_grad(float z) {
   const float t = z * z;
-  const float e = __builtin_amdgcn_exp2f(fabsf(z) * fmaf(kGeluB, t, kGeluA));
+  const float e = __builtin_amdgcn_exp2f(z * fmaf(kGeluB, t, kGeluA));
   const float r = __builtin_amdgcn_rcpf(1.0f + e);
-  const float er = e * r;
-  return fmaf(z * er * r, fmaf(kGeluG3, t, kGeluG1), z >= 0.0f ? r : er);
+  return fmaf(z * fmaf(kGeluG3, t, kGeluG1) * (1.0f - r), r, r);
 }
 
 // Quantize 8 consecutive bf16 (packed in w) of a 32-element block held by a

@@ -1117,7 +1117,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         const uint32_t codes = quad_quantize8(w, sc);
         if constexpr (QLDS) *(uint32_t*)(qbuf + (32 * i + rl) * 64 + seg * 4) = codes;
         else __builtin_amdgcn_raw_buffer_store_b32((int)codes, r_q, inb ? (uint32_t)gr * (NO / 2) + gc / 2 : kOobOffset, 0, 0);
-        if ((lane & 3) == 0) sbuf[(32 * i + rl) * 4 + (seg >> 2)] = (uint8_t)sc;
+        sbuf[(32 * i + rl) * 4 + (seg >> 2)] = (uint8_t)sc;   // the quad's four lanes write the same code
       }
       if (R2 == 0) continue;
       __builtin_amdgcn_s_waitcnt(0xc07f);
