@@ -1032,23 +1032,21 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     __syncthreads();  // all waves are done with the ring
     if (R2 > 0) {
       if constexpr (G) {
-        // four batches of two loads (left to itself the compiler waited for
-        // each load before the next); rows and columns outside read zeros
+        // all eight loads in flight at once, then the LDS writes (left to
+        // itself the compiler waited for each load before the next); rows and
+        // columns outside read zeros
         const __amdgpu_buffer_rsrc_t rp = make_rsrc(ep.proj, (uint32_t)NO * R2 * 2);
+        v4i v[8];
 #pragma unroll
-        for (int b = 0; b < 4; b++) {
-          v4i v[2];
+        for (int u = 0; u < 8; u++) {
+          const int sl = tid + 256 * u, rr = sl >> 3, cc = (sl & 7) * 8;
+          v[u] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+              rp, (n0 + rr < NO && cc < R2) ? ((uint32_t)(n0 + rr) * R2 + cc) * 2 : kOobOffset, 0, 0));
+        }
 #pragma unroll
-          for (int u = 0; u < 2; u++) {
-            const int sl = tid + 256 * (2 * b + u), rr = sl >> 3, cc = (sl & 7) * 8;
-            v[u] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
-                rp, (n0 + rr < NO && cc < R2) ? ((uint32_t)(n0 + rr) * R2 + cc) * 2 : kOobOffset, 0, 0));
-          }
-#pragma unroll
-          for (int u = 0; u < 2; u++) {
-            const int sl = tid + 256 * (2 * b + u);
-            *(v4i*)(ps + (sl >> 3) * PS1 + (sl & 7) * 8) = v[u];
-          }
+        for (int u = 0; u < 8; u++) {
+          const int sl = tid + 256 * u;
+          *(v4i*)(ps + (sl >> 3) * PS1 + (sl & 7) * 8) = v[u];
         }
       } else {
 #pragma unroll
