@@ -48,7 +48,10 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps before the timed ones (default: 200 for flux_qkv, 100 for flux_mlp, 20 for "
+                         "flux_single and the --ablation / --numerics modes, 3 for flux_stack and --dit; the clock "
+                         "takes some 30 ms of back-to-back steps to settle)")
     ap.add_argument("--workload", default="flux_qkv", choices=["flux_qkv", "flux_mlp", "flux_single", "flux_stack"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -849,9 +852,15 @@ def main():
         stop_clock_sampler(sampler, sample_path)
 
 
+DEFAULT_WARMUP = {"flux_qkv": 200, "flux_mlp": 100, "flux_single": 20, "flux_stack": 3}
+
+
 def run(args, sample_path):
     import torch
     from paper_2607_05711_amd import _lib, gen
+
+    if args.warmup is None:
+        args.warmup = 3 if args.dit else 20 if (args.ablation or args.numerics) else DEFAULT_WARMUP[args.workload]
 
     _lib.load()
     dev = torch.device("cuda:0")
