@@ -981,12 +981,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
     constexpr int PSLICE = G ? 256 * PS1 * 2 : 64 * PS2 * 2;
     uint8_t* stg = lds + wave * STG;
     uint16_t* ps = (uint16_t*)(lds + 4 * STG);
-    // This wave's E8M0 codes (128 rows x 4 blocks) and, for EPI_GELU, its
-    // E2M1 codes (128 rows x 64 bytes), written out once after the passes.
-    constexpr bool QLDS = G;
+    // This wave's E8M0 codes (128 rows x 4 blocks) and E2M1 codes (128 rows
+    // x 64 bytes), written out once after the passes.
     uint8_t* sbuf = lds + 4 * STG + PSLICE + wave * 512;
     uint8_t* qbuf = lds + 4 * STG + PSLICE + 4 * 512 + wave * (128 * 64);
-    static_assert(4 * STG + PSLICE + 4 * 512 + (QLDS ? 4 * 128 * 64 : 0) <= NSLOT * SLOT, "epilogue LDS");
+    static_assert(4 * STG + PSLICE + 4 * 512 + 4 * 128 * 64 <= NSLOT * SLOT, "epilogue LDS");
     // After the passes and the code flush, the projection partials of the two
     // waves that share rows are added through four [128 rows][64] fp32
     // regions at the start of LDS.
@@ -1113,8 +1112,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         *(v4i*)(srow + seg * 16) = wv;   // bf16 result in place (for the projection)
         uint32_t sc;
         const uint32_t codes = quad_quantize8(w, sc);
-        if constexpr (QLDS) *(uint32_t*)(qbuf + (32 * i + rl) * 64 + seg * 4) = codes;
-        else __builtin_amdgcn_raw_buffer_store_b32((int)codes, r_q, inb ? (uint32_t)gr * (NO / 2) + gc / 2 : kOobOffset, 0, 0);
+        *(uint32_t*)(qbuf + (32 * i + rl) * 64 + seg * 4) = codes;
         sbuf[(32 * i + rl) * 4 + (seg >> 2)] = (uint8_t)sc;   // the quad's four lanes write the same code
       }
       if (R2 == 0) continue;
@@ -1148,9 +1146,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp4_pipe(const uint8_t* __restr
         for (int t = 0; t < 2; t++) acc[i][t] = mfma_bf16_32x32x16(fa[ks & 1], fb[ks & 1][t], acc[i][t]);
       }
     }
-    // E2M1 codes (EPI_GELU): 16 bytes (32 columns) of a row per lane, all
-    // reads first, then branch-free stores (outside rows and columns dropped)
-    if constexpr (QLDS) {
+    // E2M1 codes: 16 bytes (32 columns) of a row per lane, all reads first,
+    // then branch-free stores (outside rows and columns dropped)
+    {
       v4i cq[8];
 #pragma unroll
       for (int q = 0; q < 8; q++) cq[q] = *(const v4i*)(qbuf + (16 * q + (lane >> 2)) * 64 + 16 * (lane & 3));
