@@ -945,6 +945,16 @@ def run(args, sample_path):
             out["library_gemm"] = library_gemm(torch, _lib, dev, args.seed)
         except Exception as e:   # noqa: BLE001
             out["library_gemm"] = {"error": "%s: %s" % (type(e).__name__, e)}
+        # the fusion ablations of --ablation (fused against unfused steps, and BF16 LoRA), fewer steps
+        try:
+            wq_a, ws_a, _ = _lib.ft_quantize_blockwise(d["W"], block_rows=32)
+            out["fusion_ablation"] = {
+                "flux_qkv": fusion_ablation(torch, _lib, d, wq_a, ws_a, gen.SHAPES["flux_qkv"], 20, 20),
+                "flux_mlp": mlp_ablation(torch, _lib, dev, args.seed, 20, 20)}
+            del wq_a, ws_a
+        except Exception as e:   # noqa: BLE001
+            out["fusion_ablation"] = {"error": "%s: %s" % (type(e).__name__, e)}
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         if d is None:
             shape = gen.SHAPES["flux_qkv"]
