@@ -103,13 +103,13 @@ __device__ __forceinline__ void quant_step(const v4i (&x)[4], int rw0, int rows,
   }
 }
 
-template <int RT, int MODE, int WAVES, int CW, int QM>
+template <int RT, int MODE, int WAVES, int CW, int QM, bool MC>
 __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __restrict__ src, int rows,
                                                                      int cols, uint8_t* __restrict__ codes,
                                                                      uint8_t* __restrict__ scales,
                                                                      const uint16_t* __restrict__ proj, int R,
                                                                      float* __restrict__ proj_out, float* __restrict__ parts,
-                                                                     SrKey key) {
+                                                                     SrKey key, int cpw) {
   using L = QuantLds<RT, MODE, WAVES, CW>;
   __shared__ __attribute__((aligned(16))) uint16_t lds[L::HALFWORDS];
   constexpr int NST = CW / 64;     // 64-column steps per chunk
@@ -118,137 +118,146 @@ __global__ __launch_bounds__(64 * WAVES) void k_quant_rows(const uint16_t* __res
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int rw0 = blockIdx.x * 32 * WAVES + wave * 32;  // first row of this wave
-  const int c0 = blockIdx.y * CW;
-  const int ncols = min(CW, cols - c0);
-  const int nblk = ncols >> 5;
   const int nbc = cols >> 5;
   const int lr = lane >> 3, lc = (lane & 7) * 8;     // row within an 8-row group, column within a step
-
-  // The first PF steps' loads go out right after the projection chunk's;
-  // each step, once consumed, issues the load PF steps ahead.  Rows past the end and blocks
-  // past the chunk read an in-range address; their values become zeros.
-  constexpr int PF = NST < 6 ? NST : 6;
-  v4i xv[NST][4];
-  auto issue = [&](int st) {
-    const int col = min(64 * st + lc, ncols - 8);
-#pragma unroll
-    for (int q = 0; q < 4; q++) {
-      const int row = min(rw0 + 8 * q + lr, rows - 1);
-      xv[st][q] = *(const v4i*)(src + (size_t)row * cols + c0 + col);
-    }
-  };
-  // The projection chunk is loaded first: every step's MFMAs need it, while
-  // the steps' own rows arrive one after another behind it.  It is staged
-  // in LDS as 16-byte slots, zero outside [R] x [ncols].
-  constexpr int SLOTS_PER_ROW = MODE == 1 ? RT * 4 : CW / 8;
-  constexpr int NSLOTS = L::ROWS * SLOTS_PER_ROW;
-  constexpr int PER_THREAD = MODE == 0 ? 1 : (NSLOTS + NT - 1) / NT;
-  [[maybe_unused]] uint4 v[PER_THREAD];
-  if constexpr (MODE != 0) {
-#pragma unroll
-    for (int u = 0; u < PER_THREAD; u++) {
-      const int s = tid + NT * u;
-      const int rr = s / SLOTS_PER_ROW, cc = (s % SLOTS_PER_ROW) * 8;
-      v[u] = make_uint4(0, 0, 0, 0);
-      if constexpr (MODE == 1) {  // rr = k within chunk, cc = j
-        if (s < NSLOTS && rr < ncols && cc < R) v[u] = *(const uint4*)(proj + (size_t)(c0 + rr) * R + cc);
-      } else {                    // rr = j, cc = k within chunk
-        if (s < NSLOTS && rr < R && cc < ncols) v[u] = *(const uint4*)(proj + (size_t)rr * cols + c0 + cc);
-      }
-    }
-  }
-#pragma unroll
-  for (int st = 0; st < PF; st++) issue(st);
-
-  if constexpr (MODE != 0) {
-#pragma unroll
-    for (int u = 0; u < PER_THREAD; u++) {
-      const int s = tid + NT * u;
-      if (s < NSLOTS) *(uint4*)(lds + (s / SLOTS_PER_ROW) * L::STRIDE + (s % SLOTS_PER_ROW) * 8) = v[u];
-    }
-    __syncthreads();
-  }
-
+  // This workgroup's chunks: one, or (MC) cpw consecutive ones (the last
+  // group may have fewer); the projection accumulates over all of them, so
+  // one partial per group leaves the workgroup.
+  const int j0 = MC ? blockIdx.y * cpw : blockIdx.y;
+  const int j1 = MC ? min(j0 + cpw, (cols + CW - 1) / CW) : j0 + 1;
   v16f acc[RT];
 #pragma unroll
   for (int t = 0; t < RT; t++) acc[t] = v16f{};
   FT_LDS uint16_t* xt = (FT_LDS uint16_t*)lds + L::PROJ_HW + wave * L::X_HW;  // this wave's 32x64 tile
   FT_LDS uint8_t* sc = (FT_LDS uint8_t*)((FT_LDS uint16_t*)lds + L::PROJ_HW + WAVES * L::X_HW + wave * L::SC_HW);
   const int r32 = lane & 31, h = lane >> 5;
-  // code bytes of this lane's rows 8q + lr at the step's first column (steps add 32 bytes)
-  uint8_t* cptr[4];
-#pragma unroll
-  for (int q = 0; q < 4; q++) cptr[q] = codes + (size_t)(rw0 + 8 * q + lr) * (cols >> 1) + ((c0 + lc) >> 1);
-  auto store = [&](int q, int st, uint32_t o) { *(uint32_t*)(cptr[q] + 32 * st) = o; };
 
-#pragma unroll
-  for (int st = 0; st < NST; st++) {
-    if (2 * st >= nblk) break;  // uniform across the workgroup
-    if (st + PF < NST) issue(st + PF);
-    const int blk = 2 * st + (lane >> 2 & 1);           // this lane's block within the chunk
-    const bool col_ok = blk < nblk;
-    // interior (every row of the wave and both blocks of the step in range):
-    // no masking; the edge path zeroes what lies outside
-    const uint64_t idx0 = (uint64_t)(rw0 + lr) * cols + c0 + 64 * st + lc;
-    if (rw0 + 32 > rows || 2 * st + 2 > nblk)
-      quant_step<true, MODE != 0, QM>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt, key,
-                                      idx0, 8ull * cols);
-    else
-      quant_step<false, MODE != 0, QM>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt, key,
-                                       idx0, 8ull * cols);
+  for (int jc = j0; jc < j1; jc++) {
+    const int c0 = jc * CW;
+    const int ncols = min(CW, cols - c0);
+    const int nblk = ncols >> 5;
+    if (jc > j0) __syncthreads();   // every wave is done with the previous chunk's projection slice
 
+    // The first PF steps' loads go out right after the projection chunk's;
+    // each step, once consumed, issues the load PF steps ahead.  Rows past the end and blocks
+    // past the chunk read an in-range address; their values become zeros.
+    constexpr int PF = NST < (MC ? 4 : 6) ? NST : (MC ? 4 : 6);   // MC: fewer steps in flight (registers)
+    v4i xv[NST][4];
+    auto issue = [&](int st) {
+      const int col = min(64 * st + lc, ncols - 8);
+#pragma unroll
+      for (int q = 0; q < 4; q++) {
+        const int row = min(rw0 + 8 * q + lr, rows - 1);
+        xv[st][q] = *(const v4i*)(src + (size_t)row * cols + c0 + col);
+      }
+    };
+    // The projection chunk is loaded first: every step's MFMAs need it, while
+    // the steps' own rows arrive one after another behind it.  It is staged
+    // in LDS as 16-byte slots, zero outside [R] x [ncols].
+    constexpr int SLOTS_PER_ROW = MODE == 1 ? RT * 4 : CW / 8;
+    constexpr int NSLOTS = L::ROWS * SLOTS_PER_ROW;
+    constexpr int PER_THREAD = MODE == 0 ? 1 : (NSLOTS + NT - 1) / NT;
+    [[maybe_unused]] uint4 v[PER_THREAD];
     if constexpr (MODE != 0) {
-      const int g16 = lane >> 4, t16 = lane & 15;
 #pragma unroll
-      for (int kk = 0; kk < 4; kk++) {
-        const v8bf a = __builtin_bit_cast(v8bf, *(const FT_LDS v4i*)(xt + r32 * QR_XSTRIDE + 16 * kk + 8 * h));
-        const int kloc = 64 * st + 16 * kk + 8 * h;  // chunk position of this lane's 8 elements
-#pragma unroll
-        for (int t = 0; t < RT; t++) {
-          v8bf b;
-          if constexpr (MODE == 2) {
-            const int j = t * 32 + r32;
-            b = __builtin_bit_cast(v8bf, *(const FT_LDS v4i*)((FT_LDS uint16_t*)lds + j * L::STRIDE + kloc));
-          } else {
-            // group g16 covers columns t*32 + 16*(g16&1) + [0,16), reduction rows kloc..kloc+7
-            const int jj = t16 >> 2, qq = t16 & 3;
-            const int col = t * 32 + 16 * (g16 & 1) + 4 * qq;
-            const FT_LDS uint16_t* base = (FT_LDS uint16_t*)lds + (kloc + jj) * L::STRIDE + col;
-            v4s lo = lds_read_tr16(base);
-            v4s hi = lds_read_tr16(base + 4 * L::STRIDE);
-            b = make_v8bf(lo, hi);
-          }
-          acc[t] = mfma_bf16_32x32x16(a, b, acc[t]);
+      for (int u = 0; u < PER_THREAD; u++) {
+        const int s = tid + NT * u;
+        const int rr = s / SLOTS_PER_ROW, cc = (s % SLOTS_PER_ROW) * 8;
+        v[u] = make_uint4(0, 0, 0, 0);
+        if constexpr (MODE == 1) {  // rr = k within chunk, cc = j
+          if (s < NSLOTS && rr < ncols && cc < R) v[u] = *(const uint4*)(proj + (size_t)(c0 + rr) * R + cc);
+        } else {                    // rr = j, cc = k within chunk
+          if (s < NSLOTS && rr < R && cc < ncols) v[u] = *(const uint4*)(proj + (size_t)rr * cols + c0 + cc);
         }
       }
     }
-  }
-
-  // scales: each row's bytes of this chunk are contiguous; 4-byte stores when
-  // rows and the chunk start are 4-byte aligned, else bytes
-  {
-    constexpr int DW = L::SC_ROW / 4;   // dwords per staged row
-    const bool al = (nbc & 3) == 0 && ((c0 >> 5) & 3) == 0;
 #pragma unroll
-    for (int d0 = 0; d0 < 32 * DW; d0 += 64) {
-      const int d = d0 + lane;
-      const int rr = d / DW, dw = d % DW;
-      const int row = rw0 + rr;
-      if (d < 32 * DW && row < rows && 4 * dw < nblk) {
-        uint8_t* dst = scales + (size_t)row * nbc + (c0 >> 5) + 4 * dw;
-        const FT_LDS uint8_t* srcb = sc + rr * L::SC_ROW + 4 * dw;
-        if (al && 4 * dw + 4 <= nblk) {
-          *(uint32_t*)dst = *(const FT_LDS uint32_t*)srcb;
-        } else {
-          for (int b = 0; b < 4 && 4 * dw + b < nblk; b++) dst[b] = srcb[b];
+    for (int st = 0; st < PF; st++) issue(st);
+
+    if constexpr (MODE != 0) {
+#pragma unroll
+      for (int u = 0; u < PER_THREAD; u++) {
+        const int s = tid + NT * u;
+        if (s < NSLOTS) *(uint4*)(lds + (s / SLOTS_PER_ROW) * L::STRIDE + (s % SLOTS_PER_ROW) * 8) = v[u];
+      }
+      __syncthreads();
+    }
+
+    // code bytes of this lane's rows 8q + lr at the step's first column (steps add 32 bytes)
+    uint8_t* cptr[4];
+#pragma unroll
+    for (int q = 0; q < 4; q++) cptr[q] = codes + (size_t)(rw0 + 8 * q + lr) * (cols >> 1) + ((c0 + lc) >> 1);
+    auto store = [&](int q, int st, uint32_t o) { *(uint32_t*)(cptr[q] + 32 * st) = o; };
+
+#pragma unroll
+    for (int st = 0; st < NST; st++) {
+      if (2 * st >= nblk) break;  // uniform across the workgroup
+      if (st + PF < NST) issue(st + PF);
+      const int blk = 2 * st + (lane >> 2 & 1);           // this lane's block within the chunk
+      const bool col_ok = blk < nblk;
+      // interior (every row of the wave and both blocks of the step in range):
+      // no masking; the edge path zeroes what lies outside
+      const uint64_t idx0 = (uint64_t)(rw0 + lr) * cols + c0 + 64 * st + lc;
+      if (rw0 + 32 > rows || 2 * st + 2 > nblk)
+        quant_step<true, MODE != 0, QM>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt, key,
+                                        idx0, 8ull * cols);
+      else
+        quant_step<false, MODE != 0, QM>(xv[st], rw0, rows, col_ok, lr, lc, lane, store, st, sc, L::SC_ROW, xt, key,
+                                         idx0, 8ull * cols);
+
+      if constexpr (MODE != 0) {
+        const int g16 = lane >> 4, t16 = lane & 15;
+#pragma unroll
+        for (int kk = 0; kk < 4; kk++) {
+          const v8bf a = __builtin_bit_cast(v8bf, *(const FT_LDS v4i*)(xt + r32 * QR_XSTRIDE + 16 * kk + 8 * h));
+          const int kloc = 64 * st + 16 * kk + 8 * h;  // chunk position of this lane's 8 elements
+#pragma unroll
+          for (int t = 0; t < RT; t++) {
+            v8bf b;
+            if constexpr (MODE == 2) {
+              const int j = t * 32 + r32;
+              b = __builtin_bit_cast(v8bf, *(const FT_LDS v4i*)((FT_LDS uint16_t*)lds + j * L::STRIDE + kloc));
+            } else {
+              // group g16 covers columns t*32 + 16*(g16&1) + [0,16), reduction rows kloc..kloc+7
+              const int jj = t16 >> 2, qq = t16 & 3;
+              const int col = t * 32 + 16 * (g16 & 1) + 4 * qq;
+              const FT_LDS uint16_t* base = (FT_LDS uint16_t*)lds + (kloc + jj) * L::STRIDE + col;
+              v4s lo = lds_read_tr16(base);
+              v4s hi = lds_read_tr16(base + 4 * L::STRIDE);
+              b = make_v8bf(lo, hi);
+            }
+            acc[t] = mfma_bf16_32x32x16(a, b, acc[t]);
+          }
+        }
+      }
+    }
+
+    // scales: each row's bytes of this chunk are contiguous; 4-byte stores when
+    // rows and the chunk start are 4-byte aligned, else bytes
+    {
+      constexpr int DW = L::SC_ROW / 4;   // dwords per staged row
+      const bool al = (nbc & 3) == 0 && ((c0 >> 5) & 3) == 0;
+#pragma unroll
+      for (int d0 = 0; d0 < 32 * DW; d0 += 64) {
+        const int d = d0 + lane;
+        const int rr = d / DW, dw = d % DW;
+        const int row = rw0 + rr;
+        if (d < 32 * DW && row < rows && 4 * dw < nblk) {
+          uint8_t* dst = scales + (size_t)row * nbc + (c0 >> 5) + 4 * dw;
+          const FT_LDS uint8_t* srcb = sc + rr * L::SC_ROW + 4 * dw;
+          if (al && 4 * dw + 4 <= nblk) {
+            *(uint32_t*)dst = *(const FT_LDS uint32_t*)srcb;
+          } else {
+            for (int b = 0; b < 4 && 4 * dw + b < nblk; b++) dst[b] = srcb[b];
+          }
         }
       }
     }
   }
 
   if constexpr (MODE != 0) {
-    // this chunk's partial (several chunks) or the projection itself (one
-    // chunk), one 32-column tile at a time through the wave's own bf16 tile
+    // this group's partial (several groups) or the projection itself (one
+    // group), one 32-column tile at a time through the wave's own bf16 tile
     // (32 rows x 36 fp32 fit its 32 x 72 halfwords), stored as row-contiguous
     // 16-byte runs: 4 stores per tile instead of 16
     static_assert(32 * 36 * 4 == L::X_HW * 2, "fp32 tile in the bf16 tile's place");
@@ -506,6 +515,18 @@ __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict_
 // partial sums, which dominate for long rows.  The [R, cols] projection
 // takes 768-column chunks (fewer partial sums; 384 and 512 are slower)
 // while the chunk fits LDS.
+// Chunks per workgroup of the chunked kernel (256-row workgroups): as many
+// as 4 while that still leaves two full rounds of workgroups (512), so that
+// long rows leave fewer partial sums (18432 x 15360 at 512 columns: 8
+// partials per row instead of 30).  Shapes with fewer than 512 workgroups
+// keep one chunk each.
+static int quant_chunks_per_wg(int rows, int cols, int cw) {
+  const size_t rb = (size_t)((rows + 255) / 256), nch = (size_t)((cols + cw - 1) / cw);
+  for (int c = 4; c > 1; c--)
+    if (rb * ((nch + c - 1) / c) >= 512) return c;
+  return 1;
+}
+
 static int quant_chunk_cols(int rows, int cols, int R, int layout) {
   if (R == 0) return 384;
   const int rt = (R + 31) / 32;
@@ -547,18 +568,25 @@ static bool quant_full_rows(int rows, int cols, int R, int layout) {
 size_t quant_rows_workspace(int rows, int cols, int R, int layout) {
   if (R == 0 || quant_full_rows(rows, cols, R, layout)) return 0;
   const int cw = quant_chunk_cols(rows, cols, R, layout);
-  const int chunks = (cols + cw - 1) / cw;
-  return chunks > 1 ? (size_t)chunks * rows * R * sizeof(float) : 0;
+  const int cpw = quant_chunks_per_wg(rows, cols, cw);
+  const int groups = ((cols + cw - 1) / cw + cpw - 1) / cpw;
+  return groups > 1 ? (size_t)groups * rows * R * sizeof(float) : 0;
 }
 
 template <int RT, int MODE, int WAVES, int CW, int QM>
 static hipError_t launch_rows_t(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
                                 const uint16_t* proj, int R, float* proj_out, float* ws, const SrKey& key,
                                 hipStream_t st) {
-  dim3 grid((rows + 32 * WAVES - 1) / (32 * WAVES), (cols + CW - 1) / CW);
+  const int cpw = MODE == 0 ? 1 : quant_chunks_per_wg(rows, cols, CW);
+  const int nch = (cols + CW - 1) / CW;
+  dim3 grid((rows + 32 * WAVES - 1) / (32 * WAVES), (nch + cpw - 1) / cpw);
   float* parts = MODE != 0 && grid.y > 1 ? ws : nullptr;
-  k_quant_rows<RT, MODE, WAVES, CW, QM><<<grid, 64 * WAVES, 0, st>>>(src, rows, cols, codes, scales, proj, R, proj_out,
-                                                                     parts, key);
+  if (cpw > 1)
+    k_quant_rows<RT, MODE, WAVES, CW, QM, true><<<grid, 64 * WAVES, 0, st>>>(src, rows, cols, codes, scales, proj, R,
+                                                                           proj_out, parts, key, cpw);
+  else
+    k_quant_rows<RT, MODE, WAVES, CW, QM, false><<<grid, 64 * WAVES, 0, st>>>(src, rows, cols, codes, scales, proj, R,
+                                                                            proj_out, parts, key, 1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !parts) return e;
   return launch_reduce_parts(parts, (int)grid.y, (size_t)rows * R, proj_out, 0, nullptr, false, st);
