@@ -63,11 +63,12 @@ def test_quantize_variants_adversarial(rule, rnd):
 @pytest.mark.parametrize("rule,rnd", MODES)
 @pytest.mark.parametrize("rows,cols,R,layout", [(300, 640, 48, 0), (2304, 4064, 64, 0), (2200, 1056, 16, 0),
                                                 (7001, 288, 64, 0), (8224, 3072, 64, 0), (300, 800, 96, 1),
-                                                (2065, 4160, 64, 1)])
+                                                (2065, 4160, 64, 1), (16640, 12288, 64, 1)])
 def test_quantize_variants_with_projection(rule, rnd, rows, cols, R, layout):
     """Every kernel path (column chunks for either projection layout, whole
-    rows per workgroup in 24- and 32-row workgroups): codes and scales as the
-    oracle's variant, projection as without the mode."""
+    rows per workgroup in 24- and 32-row workgroups, workgroups looping over
+    two chunks): codes and scales as the oracle's variant, projection as
+    without the mode."""
     rng = np.random.default_rng(rows + R)
     bits = random_rows("outliers", rows, cols, seed=rows)
     pshape = (cols, R) if layout == 0 else (R, cols)
