@@ -855,12 +855,18 @@ def main():
 DEFAULT_WARMUP = {"flux_qkv": 200, "flux_mlp": 100, "flux_single": 20, "flux_stack": 3}
 
 
+def resolve_warmup(args):
+    """Warm-up steps: --warmup if given, else the mode's default."""
+    if args.warmup is not None:
+        return args.warmup
+    return 3 if args.dit else 20 if (args.ablation or args.numerics) else DEFAULT_WARMUP[args.workload]
+
+
 def run(args, sample_path):
     import torch
     from paper_2607_05711_amd import _lib, gen
 
-    if args.warmup is None:
-        args.warmup = 3 if args.dit else 20 if (args.ablation or args.numerics) else DEFAULT_WARMUP[args.workload]
+    args.warmup = resolve_warmup(args)
 
     _lib.load()
     dev = torch.device("cuda:0")
