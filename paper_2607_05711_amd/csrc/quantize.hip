@@ -4,8 +4,9 @@
 // gradients G, FourTune Sec. 3.1 dynamic quantization), fused with the
 // low-rank down-projection of the same rows (Sec. 3.3, LoRA fusion: the
 // stabilizer and adapter branches share the input, so one pass reads it once).
-// Workgroups cover column chunks; their partial projections are summed by
-// k_reduce_parts.
+// Workgroups cover one column chunk, or (MC) a few consecutive ones with
+// the projection slice re-staged between them; their partial projections
+// are summed by k_reduce_parts.
 // k_quant_rows_fr: the same for a [cols, R] projection with whole rows per
 // workgroup, which adds its partial projections itself.
 // k_quant_tiles: 32x32 tiles of the frozen weight (Sec. 3.2), offline.
@@ -15,7 +16,8 @@
 namespace ft {
 
 // ---------------------------------------------------------------- rows
-// Workgroup = WAVES waves over 32*WAVES rows x CW columns; wave w owns rows
+// Workgroup = WAVES waves over 32*WAVES rows x CW columns (x cpw chunks with
+// MC); wave w owns rows
 // [row0 + 32w, +32).  The wave walks its columns in steps of 64.  Loads are
 // row-contiguous: load q of a step brings rows 8q..8q+7, lane l taking
 // elements [8(l%8), +8) of row 8q + l/8, so every 8 lanes read one whole
