@@ -517,15 +517,18 @@ __global__ __launch_bounds__(256) void k_quant_tiles(const uint16_t* __restrict_
 // partial sums, which dominate for long rows.  The [R, cols] projection
 // takes 768-column chunks (fewer partial sums; 384 and 512 are slower)
 // while the chunk fits LDS.
-// Chunks per workgroup of the chunked kernel (256-row workgroups): as many
-// as 4 while that still leaves two full rounds of workgroups (512), so that
-// long rows leave fewer partial sums (18432 x 15360 at 512 columns: 8
-// partials per row instead of 30).  Shapes with fewer than 512 workgroups
-// keep one chunk each.
-static int quant_chunks_per_wg(int rows, int cols, int cw) {
+// Chunks per workgroup of the chunked kernel (256-row workgroups), so that
+// long rows leave fewer partial sums: for [cols, R] as many as 6 while 384
+// workgroups remain (18432 x 15360 at 512 columns: 6 partials per row
+// instead of 30), for [R, cols] as many as 4 while 512 remain (18432 x 21504:
+// 11 instead of 42; 3 or 8 per workgroup measured slower).  Shapes with fewer
+// workgroups keep one chunk each.
+static int quant_chunks_per_wg(int rows, int cols, int cw, int layout) {
   const size_t rb = (size_t)((rows + 255) / 256), nch = (size_t)((cols + cw - 1) / cw);
-  for (int c = 4; c > 1; c--)
-    if (rb * ((nch + c - 1) / c) >= 512) return c;
+  const int cmax = layout == 0 ? 6 : 4;
+  const size_t need = layout == 0 ? 384 : 512;
+  for (int c = cmax; c > 1; c--)
+    if (rb * ((nch + c - 1) / c) >= need) return c;
   return 1;
 }
 
@@ -570,7 +573,7 @@ static bool quant_full_rows(int rows, int cols, int R, int layout) {
 size_t quant_rows_workspace(int rows, int cols, int R, int layout) {
   if (R == 0 || quant_full_rows(rows, cols, R, layout)) return 0;
   const int cw = quant_chunk_cols(rows, cols, R, layout);
-  const int cpw = quant_chunks_per_wg(rows, cols, cw);
+  const int cpw = quant_chunks_per_wg(rows, cols, cw, layout);
   const int groups = ((cols + cw - 1) / cw + cpw - 1) / cpw;
   return groups > 1 ? (size_t)groups * rows * R * sizeof(float) : 0;
 }
@@ -579,7 +582,7 @@ template <int RT, int MODE, int WAVES, int CW, int QM>
 static hipError_t launch_rows_t(const uint16_t* src, int rows, int cols, uint8_t* codes, uint8_t* scales,
                                 const uint16_t* proj, int R, float* proj_out, float* ws, const SrKey& key,
                                 hipStream_t st) {
-  const int cpw = MODE == 0 ? 1 : quant_chunks_per_wg(rows, cols, CW);
+  const int cpw = MODE == 0 ? 1 : quant_chunks_per_wg(rows, cols, CW, MODE == 1 ? 0 : 1);
   const int nch = (cols + CW - 1) / CW;
   dim3 grid((rows + 32 * WAVES - 1) / (32 * WAVES), (nch + cpw - 1) / cpw);
   float* parts = MODE != 0 && grid.y > 1 ? ws : nullptr;

@@ -86,11 +86,12 @@ def test_quantize_validation():
     assert _lib.ft_quantize_workspace_size(8224, 3072, 1, 64, 0) == 8 * 8224 * 64 * 4     # 384 otherwise
     # the widest chunk that fits LDS (512 for R = 96, 640 for R <= 64) while it still makes a full
     # round of workgroups, else as above
-    # long rows: four 512-column chunks per workgroup while two full rounds remain (30 chunks, 8 groups)
-    assert _lib.ft_quantize_workspace_size(18432, 15360, 1, 96, 0) == 8 * 18432 * 96 * 4
+    # long rows: several chunks per workgroup ([cols, R]: up to 6 while 384 workgroups remain, 30 chunks
+    # in 6 groups; [R, cols]: up to 4 while 512 remain)
+    assert _lib.ft_quantize_workspace_size(18432, 15360, 1, 96, 0) == 6 * 18432 * 96 * 4
     assert _lib.ft_quantize_workspace_size(18432, 21504, 1, 96, 1) == 11 * 18432 * 96 * 4   # [R, cols]: 42 chunks
     assert _lib.ft_quantize_workspace_size(16640, 16384, 1, 64, 1) == 8 * 16640 * 64 * 4    # 22 chunks, 3 per group
-    assert _lib.ft_quantize_workspace_size(16640, 16384, 1, 64, 0) == 9 * 16640 * 64 * 4    # 26 chunks, 3 per group
+    assert _lib.ft_quantize_workspace_size(16640, 16384, 1, 64, 0) == 6 * 16640 * 64 * 4    # 26 chunks, 5 per group
     assert _lib.ft_quantize_workspace_size(4608, 15360, 1, 64, 0) == 24 * 4608 * 64 * 4
     assert _lib.ft_quantize_workspace_size(2304, 10976, 1, 64, 0) == 29 * 2304 * 64 * 4     # 640 would make 162
     assert _lib.ft_quantize_workspace_size(18432, 3072, 1, 96, 0) == 6 * 18432 * 96 * 4

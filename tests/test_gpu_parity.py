@@ -120,10 +120,9 @@ def test_quantize_tiles_bitexact(rows, cols):
                                                 # R = 96) and with 768-column chunks and a ragged last one
                                                 (2065, 4160, 64, 1), (3000, 2080, 32, 1), (2080, 640, 48, 1),
                                                 (1000, 5152, 96, 1), (4352, 6400, 64, 1),
-                                                # workgroups looping over three chunks (two rounds of them
-                                                # remain): ragged rows, a last group of one chunk ([R, cols],
-                                                # 22 chunks of 768) or of two ([cols, R], 26 of 640), each
-                                                # with a ragged last chunk
+                                                # workgroups looping over several chunks: ragged rows, a
+                                                # last group of one ragged chunk ([R, cols]: 22 chunks of
+                                                # 768, 3 per group; [cols, R]: 26 of 640, 5 per group)
                                                 (16640, 16384, 64, 1), (16640, 16384, 64, 0)])
 def test_quantize_fused_projection(rows, cols, R, layout):
     rng = np.random.default_rng(rows + cols + R)
